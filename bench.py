@@ -1,0 +1,205 @@
+#!/usr/bin/env python3
+"""Benchmark of one BRISK-DLM decoding step on one MI355X.
+
+A step is the whole hot path over one block batch: brisk_propose_block (LM
+head + fused top-K), brisk_rerank (the prefix-conditioned corrector) and
+brisk_verify_accept (greedy verification).  Inputs are synthetic, drawn once
+on the GPU and resident in HBM before timing starts.
+
+Prints one JSON line: block positions per second, the propose stage's
+achieved HBM bandwidth (or MFMA rate) against the MI355X peak, per-stage
+times, and the CPU oracle timed on the host on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import statistics
+import sys
+import time
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+BF16_PEAK_TFLOPS = 2516.6      # dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
+METRIC = "block positions/sec (propose+rerank+verify) and % HBM/MFMA roofline"
+DEFAULT_WORKLOAD = "llada8b-b1-l32"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--graph", action="store_true", help="time hipGraph replay of the step")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def propose_cost(wl):
+    """Algorithmic bytes and flops of brisk_propose_block for one step."""
+    rows = wl.B * wl.L
+    bytes_ = 2 * wl.V * wl.d + 2 * rows * wl.d + rows * wl.K * 8
+    flops = 2 * rows * wl.d * wl.V
+    return bytes_, flops
+
+
+def cpu_baseline(blk, budget_s):
+    """The oracle, as is, on host cores: whole steps of the same workload,
+    repeated until the time budget is spent (at least one)."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle
+    from synth import PSI_FIELDS, bf16_bits
+
+    wl = blk.wl
+    H_bits, W_bits, E_bits = bf16_bits(blk.H), bf16_bits(blk.W), bf16_bits(blk.E)
+    H = oracle.bf16_to_f64(H_bits)
+    h_c = oracle.bf16_to_f64(bf16_bits(blk.h_c))
+    x0 = blk.x0.cpu().numpy().astype(np.int64)
+    ver = blk.verifier.cpu().numpy()
+    psi = {k: oracle.bf16_to_f64(bf16_bits(blk.psi[k])) for k in PSI_FIELDS}
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while True:
+        t0 = time.perf_counter()
+        cl, ci = oracle.propose_block(H_bits, W_bits, wl.K)
+        out = oracle.rerank(psi, blk.alpha, blk.b_g, H, h_c, x0, W_bits, E_bits, cl, ci, wl.B, wl.L)
+        oracle.verify_accept(out["selected"], ver)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() >= t_end or len(times) >= 5:
+            break
+    blas = [p.get("num_threads", 0) for p in threadpool_info() if p.get("user_api") == "blas"]
+    cores = max(blas) if blas else 1
+    t = statistics.median(times)
+    return {"value": wl.B * wl.L / t, "unit": "block positions/s", "cores": cores, "kind": "oracle",
+            "sample": f"{len(times)} whole step(s) of {wl.name} ({wl.B * wl.L} positions), median "
+                      f"{t:.2f} s; float64 numpy, host has {os.cpu_count()} logical CPUs"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the hot path is data parallel: see the sharding notes in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2609_33390_amd as brisk
+    import synth
+
+    wl = synth.WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    blk = synth.make_block(wl, dev)
+    corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
+    rows, K = wl.B * wl.L, wl.K
+    cl = torch.empty(rows, K, dtype=torch.float32, device=dev)
+    ci = torch.empty(rows, K, dtype=torch.int32, device=dev)
+    sel = torch.empty(wl.B, wl.L, dtype=torch.int32, device=dev)
+    acc = torch.empty(wl.B, dtype=torch.int32, device=dev)
+    cor = torch.empty(wl.B, dtype=torch.int32, device=dev)
+    ws_p = torch.empty(brisk.propose_workspace_size(rows, wl.d, wl.V, K), dtype=torch.uint8, device=dev)
+    ws_r = torch.empty(brisk.rerank_workspace_size(corr, wl.B, wl.L, K), dtype=torch.uint8, device=dev)
+
+    def propose():
+        brisk.propose_block(blk.H, blk.W, K, cand_logit=cl, cand_id=ci, workspace=ws_p)
+
+    def rest():
+        brisk.rerank(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, wl.B, wl.L, selected=sel,
+                     workspace=ws_r)
+        brisk.verify_accept(sel, blk.verifier, accept_len=acc, correction=cor)
+
+    for _ in range(args.warmup):
+        propose()
+        rest()
+    torch.cuda.synchronize()
+
+    n = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(n)]
+    if args.graph:
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            with torch.cuda.graph(g, stream=s):
+                propose()
+                rest()
+        torch.cuda.synchronize()
+        for _ in range(args.warmup):
+            g.replay()
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record()
+        for _ in range(n):
+            g.replay()
+        t1.record()
+        torch.cuda.synchronize()
+        total_ms = t0.elapsed_time(t1)
+        # propose-only timing outside the graph for the roofline figure
+        for i in range(n):
+            ev[i][0].record()
+            propose()
+            ev[i][1].record()
+        torch.cuda.synchronize()
+        prop_ms = [ev[i][0].elapsed_time(ev[i][1]) for i in range(n)]
+        rest_ms = [float("nan")]
+    else:
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        t0.record()
+        for i in range(n):
+            ev[i][0].record()
+            propose()
+            ev[i][1].record()
+            rest()
+            ev[i][2].record()
+        t1.record()
+        torch.cuda.synchronize()
+        total_ms = t0.elapsed_time(t1)
+        prop_ms = [ev[i][0].elapsed_time(ev[i][1]) for i in range(n)]
+        rest_ms = [ev[i][1].elapsed_time(ev[i][2]) for i in range(n)]
+
+    ms_step = total_ms / n
+    value = rows / (ms_step * 1e-3)
+    bytes_, flops = propose_cost(wl)
+    t_prop = statistics.mean(prop_ms) * 1e-3
+    ai = flops / bytes_
+    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+    if ai < ridge:
+        achieved = bytes_ / t_prop / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBS, 4)}
+    else:
+        achieved = flops / t_prop / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4)}
+    roof["traffic"] = None
+    roof["kernel"] = "brisk_propose_block (lmhead_topk + topk_merge)"
+    roof["launch_us"] = round(t_prop * 1e6, 2)
+
+    torch.cuda.synchronize()
+    hist = torch.bincount(acc.long(), minlength=wl.L + 1).cpu().tolist()
+    res = {
+        "metric": METRIC, "value": round(value, 1), "unit": "block positions/s", "n_gpus": 1,
+        "steps": n, "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded; LLaDA/Dream-shaped random blocks, random-init corrector)",
+        "config": {"workload": wl.name, "B": wl.B, "L": wl.L, "d": wl.d, "V": wl.V, "K": wl.K,
+                   "r": wl.r, "timing": "hipGraph replay" if args.graph else "eager, one stream"},
+        "roofline": roof,
+        "stages_ms": {"propose": round(statistics.mean(prop_ms), 5),
+                      "rerank+verify": round(statistics.mean(rest_ms), 5) if not args.graph else None},
+        "accept_hist": hist,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(blk, args.cpu_budget_s)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,172 @@
+/*
+ * brisk.h - C ABI of the BRISK-DLM decoding hot path on MI355X (gfx950).
+ *
+ * One decoding step of the paper's prefix-conditioned proposal selection
+ * (Section 3.3, Algorithm 1(b)) in three calls:
+ *
+ *   brisk_propose_block  LM-head projection of every masked position's hidden
+ *                        state and its ordered top-K candidate set;
+ *   brisk_rerank         the corrector that re-scores those candidates left to
+ *                        right, conditioned on the tokens already selected;
+ *   brisk_verify_accept  greedy verification: accepted-prefix length and the
+ *                        correction token of each block.
+ *
+ * Conventions shared by every entry point
+ *   - Every pointer argument is a DEVICE pointer owned by the caller, except
+ *     the brisk_corrector struct itself (host memory, read during the call)
+ *     and the size out-parameters.  The library allocates nothing, keeps no
+ *     global state and is reentrant; calls on different streams are safe when
+ *     their workspaces and outputs differ.
+ *   - bf16 tensors are passed as uint16_t bit patterns; all matrices are
+ *     row-major and densely packed (row stride = row length).
+ *   - Rows of a block are numbered r = b * L + (i - 1) for sequence b and
+ *     in-block position i = 1..L.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Work is queued
+ *     on it asynchronously; nothing synchronises.
+ *   - Every call returns a brisk_status.  Arguments are validated on the host
+ *     before any HIP call: on an error return nothing has been launched and no
+ *     output has been touched.  BRISK_ERR_HIP reports a failed launch.
+ *   - Token ids read from device memory (candidate ids, anchor tokens) are
+ *     clamped into [0, V) before they address a table, so a bad id cannot make
+ *     a kernel read out of bounds; the results for such a row are unspecified.
+ *   - Pointers must be 16-byte aligned and d a multiple of 8, otherwise
+ *     BRISK_ERR_UNSUPPORTED.
+ */
+#ifndef BRISK_H_
+#define BRISK_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BRISK_OK = 0,
+  BRISK_ERR_NULL = -1,        /* a required pointer is NULL                   */
+  BRISK_ERR_SHAPE = -2,       /* a size is out of range or inconsistent        */
+  BRISK_ERR_UNSUPPORTED = -3, /* alignment / divisibility the kernels need     */
+  BRISK_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required    */
+  BRISK_ERR_HIP = -5          /* a HIP launch failed                           */
+} brisk_status;
+
+/* Static, NUL-terminated description of a status code. */
+const char* brisk_status_str(int status);
+
+/* Library ABI version (bumped on any signature or struct change). */
+int brisk_abi_version(void);
+
+/*
+ * Corrector parameters psi (Section 3.3 Eq. inference_head_state and
+ * Eq. candidate_residual; Appendix "Candidate-Refinement Head Details",
+ * Eq. head_residual_logits and the head configuration table).  All tensor
+ * pointers are device bf16 bit patterns, row-major:
+ *
+ *   u_0      = tanh(A_h h_c + A_e E(x_0))
+ *   x_hat_i  = [P_h m_i ; P_e E(x_{i-1}) ; pos_emb[i-1] ; P_phi phi_i]
+ *   z        = sigmoid(W_z x_hat_i),  u_i = (1 - z) * u_{i-1} + z * (W_h x_hat_i)
+ *   gamma_i  = sigmoid(alpha) * sigmoid(w_g . [u_i ; phi_i] + b_g)
+ *   l~_{i,k} = l_{i,k} + gamma_i * <W_s u_i, W_c E_out(v_{i,k})>
+ *
+ * with phi_i = [top1-top2, top1-top4, 1[x_{i-1} = top1], 1[x_{i-1} in top4],
+ * top1 - l_i(x_{i-1})] from the position's ordered candidates and E_out the
+ * LM head.  Dimension limits: d_state in [1, 512], d_hproj, d_tproj, rank in
+ * [1, 256], d_pos, d_feat in [1, 64], max_L >= 1.
+ */
+typedef struct brisk_corrector {
+  int32_t d_state, d_hproj, d_tproj, d_pos, d_feat, rank, max_L;
+  const uint16_t* A_h;      /* [d_state, d]                               */
+  const uint16_t* A_e;      /* [d_state, d]                               */
+  const uint16_t* P_h;      /* [d_hproj, d]                               */
+  const uint16_t* P_e;      /* [d_tproj, d]                               */
+  const uint16_t* pos_emb;  /* [max_L, d_pos]                             */
+  const uint16_t* P_phi;    /* [d_feat, 5]                                */
+  const uint16_t* W_z;      /* [d_state, d_in], d_in = d_hproj+d_tproj+d_pos+d_feat */
+  const uint16_t* W_h;      /* [d_state, d_in]                            */
+  const uint16_t* W_s;      /* [rank, d_state]                            */
+  const uint16_t* W_c;      /* [rank, d]                                  */
+  const uint16_t* w_g;      /* [d_state + 5]                              */
+  float alpha;              /* gate scale logit (host value)               */
+  float b_g;                /* gate bias (host value)                      */
+} brisk_corrector;
+
+/*
+ * Workspace bytes brisk_propose_block needs for this shape (written to *bytes).
+ * Returns BRISK_ERR_SHAPE / BRISK_ERR_NULL on bad arguments.
+ */
+int brisk_propose_workspace_size(int32_t rows, int32_t d, int32_t V, int32_t K, size_t* bytes);
+
+/*
+ * Candidate construction C_i = TopK(q_i, K) (Section 3.3; Appendix head
+ * details; Algorithm 1(b) first step and loop head).  Computes the proposal
+ * logits l[r, v] = sum_k hidden[r, k] * lm_head[v, k] (bf16 inputs, fp32
+ * accumulation; the [rows, V] logits never reach memory) and returns the K
+ * largest per row, ordered by logit descending and, among equal logits, by
+ * token id ascending.  Top-K of the softmax q equals top-K of the logits.
+ *
+ *   hidden      [rows, d]  bf16   masked-position hidden states m_i
+ *   lm_head     [V, d]     bf16   frozen LM head (output vocabulary rows)
+ *   cand_logit  [rows, K]  fp32   out: candidate logits, descending
+ *   cand_id     [rows, K]  int32  out: candidate token ids
+ *   ws          device scratch of at least brisk_propose_workspace_size bytes
+ *
+ * Limits: 1 <= rows, 8 <= d <= 65536, 1 <= K <= 64, K <= V <= 2^31 - 1.
+ */
+int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head,
+                        int32_t rows, int32_t d, int32_t V, int32_t K,
+                        float* cand_logit, int32_t* cand_id,
+                        void* ws, size_t ws_bytes, void* stream);
+
+/* Workspace bytes brisk_rerank needs (written to *bytes). */
+int brisk_rerank_workspace_size(const brisk_corrector* c, int32_t B, int32_t L, int32_t K,
+                                size_t* bytes);
+
+/*
+ * Prefix-conditioned rerank of the candidates (Section 3.3; Appendix head
+ * details; Algorithm 1(b) loop): steps the corrector over i = 1..L for every
+ * sequence, feeding the token selected at i-1 (x_0 at i = 1) into step i, and
+ * selects x_i = the candidate with the largest refined logit (the smallest
+ * candidate index on ties).
+ *
+ *   c           host struct of device parameter pointers (see above)
+ *   hidden      [B*L, d] bf16   m_i
+ *   ctx_hidden  [B, d]   bf16   h_c
+ *   anchor_tok  [B]      int32  x_0, the token preceding each block
+ *   lm_head     [V, d]   bf16   E_out (the same matrix brisk_propose_block used)
+ *   tok_embed   [V, d]   bf16   E, the input token embedding
+ *   cand_logit, cand_id [B*L, K] the candidate sets from brisk_propose_block
+ *   selected    [B, L]   int32  out: x_{1..L}
+ *   refined     [B*L, K] fp32   out, nullable: refined logits l~
+ *   gamma       [B*L]    fp32   out, nullable: gate gamma_i
+ *   resid       [B*L, K] fp32   out, nullable: residual <W_s u_i, W_c E_out(v)>
+ *
+ * Limits: 4 <= K <= 64 (the features read the top-4), 1 <= L <= max_L.
+ */
+int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                 const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                 const float* cand_logit, const int32_t* cand_id,
+                 int32_t B, int32_t L, int32_t K, int32_t d, int32_t V,
+                 int32_t* selected, float* refined, float* gamma, float* resid,
+                 void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Greedy verification (Section 2.2 accepted prefix; Section 3.3 speculative
+ * acceptance, temperature-zero case; Algorithm 1(b) verify and commit):
+ * accept_len[b] = number of leading positions i with proposal[b, i] ==
+ * verifier[b, i], in [0, L]; correction[b] = verifier[b, accept_len[b]] when
+ * accept_len[b] < L, else -1.
+ *
+ *   proposal    [B, L] int32   proposed tokens x_{1..L}
+ *   verifier    [B, L] int32   the verifier's argmax tokens
+ *   accept_len  [B]    int32   out
+ *   correction  [B]    int32   out, nullable
+ */
+int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,
+                        int32_t* accept_len, int32_t* correction, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BRISK_H_ */

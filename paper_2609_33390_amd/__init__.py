@@ -1,0 +1,264 @@
+"""BRISK-DLM decoding hot path on MI355X (gfx950).
+
+Thin Python binding of ``libbrisk.so``: it checks tensor metadata, allocates
+outputs and workspaces with torch, and passes raw device pointers and the
+current HIP stream to the C ABI declared in ``include/brisk.h``.  Every step of
+the computation runs in the library's HIP kernels; there is no CPU fallback,
+and a missing or unloadable library raises.
+
+Entry points (same names as the C ABI):
+
+* :func:`propose_block` - LM-head logits and ordered top-K candidates;
+* :func:`rerank` - the prefix-conditioned corrector over the candidates;
+* :func:`verify_accept` - greedy verification: accept length and correction.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import threading
+from typing import Dict, Optional, Tuple
+
+import torch
+
+__all__ = ["BriskError", "Corrector", "propose_block", "rerank", "verify_accept", "lib",
+           "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
+ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
+               "brisk_propose_block", "brisk_rerank_workspace_size", "brisk_rerank",
+               "brisk_verify_accept")
+PSI_FIELDS = ("A_h", "A_e", "P_h", "P_e", "pos_emb", "P_phi", "W_z", "W_h", "W_s", "W_c", "w_g")
+
+_p = ctypes.c_void_p
+_i32 = ctypes.c_int32
+_sz = ctypes.c_size_t
+
+
+class BriskError(RuntimeError):
+    """A non-zero status returned by the library."""
+
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: status {status} ({_status_str(status)})")
+
+
+class _CorrectorC(ctypes.Structure):
+    _fields_ = ([(n, _i32) for n in ("d_state", "d_hproj", "d_tproj", "d_pos", "d_feat", "rank", "max_L")]
+                + [(n, _p) for n in PSI_FIELDS]
+                + [("alpha", ctypes.c_float), ("b_g", ctypes.c_float)])
+
+
+_lib = None
+_lib_lock = threading.Lock()
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    with _lib_lock:
+        if _lib is None:
+            if not os.path.exists(LIB_PATH):
+                raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                                   "`python -m paper_2609_33390_amd.build`")
+            L = ctypes.CDLL(LIB_PATH)
+            L.brisk_status_str.restype = ctypes.c_char_p
+            L.brisk_status_str.argtypes = [ctypes.c_int]
+            L.brisk_abi_version.restype = ctypes.c_int
+            L.brisk_abi_version.argtypes = []
+            L.brisk_propose_workspace_size.restype = ctypes.c_int
+            L.brisk_propose_workspace_size.argtypes = [_i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
+            L.brisk_propose_block.restype = ctypes.c_int
+            L.brisk_propose_block.argtypes = [_p, _p, _i32, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
+            L.brisk_rerank_workspace_size.restype = ctypes.c_int
+            L.brisk_rerank_workspace_size.argtypes = [ctypes.POINTER(_CorrectorC), _i32, _i32, _i32,
+                                                      ctypes.POINTER(_sz)]
+            L.brisk_rerank.restype = ctypes.c_int
+            L.brisk_rerank.argtypes = [ctypes.POINTER(_CorrectorC), _p, _p, _p, _p, _p, _p, _p,
+                                       _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _sz, _p]
+            L.brisk_verify_accept.restype = ctypes.c_int
+            L.brisk_verify_accept.argtypes = [_p, _p, _i32, _i32, _p, _p, _p]
+            _lib = L
+        return _lib
+
+
+def _status_str(status: int) -> str:
+    try:
+        return lib().brisk_status_str(status).decode()
+    except Exception:  # pragma: no cover - message only
+        return "?"
+
+
+def _check(status: int, where: str) -> None:
+    if status != 0:
+        raise BriskError(status, where)
+
+
+def _dev_tensor(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: int) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on a HIP device, got {t.device}")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream_ptr(device: torch.device, stream) -> Optional[int]:
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+_ws: Dict[Tuple[int, str], torch.Tensor] = {}
+
+
+def _workspace(device: torch.device, nbytes: int, tag: str) -> torch.Tensor:
+    """Per-device cached scratch buffer (grown on demand).  Callers that run the
+    same entry point concurrently on several streams must pass their own."""
+    key = (device.index if device.index is not None else torch.cuda.current_device(), tag)
+    buf = _ws.get(key)
+    if buf is None or buf.numel() < nbytes:
+        buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device=device)
+        _ws[key] = buf
+    return buf
+
+
+# ----------------------------------------------------------------- propose
+def propose_workspace_size(rows: int, d: int, V: int, K: int) -> int:
+    out = _sz()
+    _check(lib().brisk_propose_workspace_size(rows, d, V, K, ctypes.byref(out)),
+           "brisk_propose_workspace_size")
+    return out.value
+
+
+def propose_block(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, *,
+                  cand_logit: Optional[torch.Tensor] = None, cand_id: Optional[torch.Tensor] = None,
+                  workspace: Optional[torch.Tensor] = None, stream=None
+                  ) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Ordered top-K candidates of every row: (cand_logit [rows,K] fp32, cand_id [rows,K] int32)."""
+    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
+    rows, d = hidden.shape
+    V = lm_head.shape[0]
+    if lm_head.shape[1] != d:
+        raise ValueError("hidden and lm_head disagree on d")
+    dev = hidden.device
+    if cand_logit is None:
+        cand_logit = torch.empty(rows, K, dtype=torch.float32, device=dev)
+    if cand_id is None:
+        cand_id = torch.empty(rows, K, dtype=torch.int32, device=dev)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
+    need = propose_workspace_size(rows, d, V, K)
+    ws = workspace if workspace is not None else _workspace(dev, need, "propose")
+    st = lib().brisk_propose_block(_ptr(hidden), _ptr(lm_head), rows, d, V, K, _ptr(cand_logit),
+                                   _ptr(cand_id), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _stream_ptr(dev, stream))
+    _check(st, "brisk_propose_block")
+    return cand_logit, cand_id
+
+
+# ----------------------------------------------------------------- rerank
+class Corrector:
+    """Corrector parameters psi: bf16 device tensors plus the two gate scalars."""
+
+    def __init__(self, tensors: Dict[str, torch.Tensor], alpha: float, b_g: float):
+        missing = [n for n in PSI_FIELDS if n not in tensors]
+        if missing:
+            raise ValueError(f"missing corrector tensors: {missing}")
+        self.t = {n: tensors[n].contiguous() for n in PSI_FIELDS}
+        for n, v in self.t.items():
+            _dev_tensor(v, n, torch.bfloat16, 1 if n == "w_g" else 2)
+        self.alpha, self.b_g = float(alpha), float(b_g)
+        ds = self.t["A_h"].shape[0]
+        self.dims = dict(d_state=ds, d_hproj=self.t["P_h"].shape[0], d_tproj=self.t["P_e"].shape[0],
+                         d_pos=self.t["pos_emb"].shape[1], d_feat=self.t["P_phi"].shape[0],
+                         rank=self.t["W_s"].shape[0], max_L=self.t["pos_emb"].shape[0])
+        self._c = _CorrectorC(**self.dims, **{n: _ptr(self.t[n]) for n in PSI_FIELDS},
+                              alpha=self.alpha, b_g=self.b_g)
+
+    @property
+    def c_struct(self) -> _CorrectorC:
+        return self._c
+
+
+def rerank_workspace_size(corr: Corrector, B: int, L: int, K: int) -> int:
+    out = _sz()
+    _check(lib().brisk_rerank_workspace_size(ctypes.byref(corr.c_struct), B, L, K, ctypes.byref(out)),
+           "brisk_rerank_workspace_size")
+    return out.value
+
+
+def rerank(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anchor_tok: torch.Tensor,
+           lm_head: torch.Tensor, tok_embed: torch.Tensor, cand_logit: torch.Tensor,
+           cand_id: torch.Tensor, B: int, L: int, *, want_scores: bool = False,
+           selected: Optional[torch.Tensor] = None, refined: Optional[torch.Tensor] = None,
+           gamma: Optional[torch.Tensor] = None, resid: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
+    """Run the corrector; returns {"selected": [B,L] int32} plus "refined", "gamma",
+    "resid" when ``want_scores`` (or when the caller passes those buffers)."""
+    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
+    _dev_tensor(ctx_hidden, "ctx_hidden", torch.bfloat16, 2)
+    _dev_tensor(anchor_tok, "anchor_tok", torch.int32, 1)
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
+    _dev_tensor(tok_embed, "tok_embed", torch.bfloat16, 2)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
+    rows, d = hidden.shape
+    V, K = lm_head.shape[0], cand_id.shape[1]
+    if rows != B * L or cand_id.shape[0] != rows or tuple(cand_logit.shape) != (rows, K):
+        raise ValueError("row counts disagree with B*L")
+    if ctx_hidden.shape != (B, d) or anchor_tok.shape[0] != B or tok_embed.shape != lm_head.shape:
+        raise ValueError("context / anchor / embedding shapes disagree")
+    dev = hidden.device
+    if selected is None:
+        selected = torch.empty(B, L, dtype=torch.int32, device=dev)
+    if want_scores:
+        if refined is None:
+            refined = torch.empty(rows, K, dtype=torch.float32, device=dev)
+        if gamma is None:
+            gamma = torch.empty(rows, dtype=torch.float32, device=dev)
+        if resid is None:
+            resid = torch.empty(rows, K, dtype=torch.float32, device=dev)
+    need = rerank_workspace_size(corr, B, L, K)
+    ws = workspace if workspace is not None else _workspace(dev, need, "rerank")
+    st = lib().brisk_rerank(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
+                            _ptr(anchor_tok), _ptr(lm_head), _ptr(tok_embed), _ptr(cand_logit),
+                            _ptr(cand_id), B, L, K, d, V, _ptr(selected), _ptr(refined), _ptr(gamma),
+                            _ptr(resid), _ptr(ws), ws.numel() * ws.element_size(),
+                            _stream_ptr(dev, stream))
+    _check(st, "brisk_rerank")
+    out = {"selected": selected}
+    for k, v in (("refined", refined), ("gamma", gamma), ("resid", resid)):
+        if v is not None:
+            out[k] = v
+    return out
+
+
+# ----------------------------------------------------------------- verify
+def verify_accept(proposal: torch.Tensor, verifier: torch.Tensor, *,
+                  accept_len: Optional[torch.Tensor] = None, correction: Optional[torch.Tensor] = None,
+                  stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """(accept_len [B] int32, correction [B] int32; -1 where the block is fully accepted)."""
+    _dev_tensor(proposal, "proposal", torch.int32, 2)
+    _dev_tensor(verifier, "verifier", torch.int32, 2)
+    if proposal.shape != verifier.shape:
+        raise ValueError("proposal and verifier shapes differ")
+    B, L = proposal.shape
+    dev = proposal.device
+    if accept_len is None:
+        accept_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if correction is None:
+        correction = torch.empty(B, dtype=torch.int32, device=dev)
+    st = lib().brisk_verify_accept(_ptr(proposal), _ptr(verifier), B, L, _ptr(accept_len),
+                                   _ptr(correction), _stream_ptr(dev, stream))
+    _check(st, "brisk_verify_accept")
+    return accept_len, correction

@@ -1,0 +1,147 @@
+// C ABI of the decoding hot path: argument validation, workspace sizing and
+// kernel launches.  Every check runs on the host before the first HIP call, so
+// an error return has launched nothing and touched no output.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "../../include/brisk.h"
+#include "kernels.h"
+
+namespace {
+
+constexpr int kAbiVersion = 1;
+constexpr int32_t kMaxRows = 1 << 20;
+constexpr int32_t kMaxD = 65536;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
+bool aligned2(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 1u) == 0; }
+
+int propose_check(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
+                  int32_t V, int32_t K, const float* cand_logit, const int32_t* cand_id) {
+  if (!hidden || !lm_head || !cand_logit || !cand_id) return BRISK_ERR_NULL;
+  if (rows < 1 || rows > kMaxRows || d < 8 || d > kMaxD || K < 1 || K > 64 || V < K)
+    return BRISK_ERR_SHAPE;
+  if (d % 8 != 0 || !aligned16(hidden) || !aligned16(lm_head) || !aligned4(cand_logit) ||
+      !aligned4(cand_id))
+    return BRISK_ERR_UNSUPPORTED;
+  return BRISK_OK;
+}
+
+int corrector_check(const brisk_corrector* c) {
+  if (!c) return BRISK_ERR_NULL;
+  if (!c->A_h || !c->A_e || !c->P_h || !c->P_e || !c->pos_emb || !c->P_phi || !c->W_z ||
+      !c->W_h || !c->W_s || !c->W_c || !c->w_g)
+    return BRISK_ERR_NULL;
+  if (c->d_state < 1 || c->d_state > 512 || c->d_hproj < 1 || c->d_hproj > 256 ||
+      c->d_tproj < 1 || c->d_tproj > 256 || c->rank < 1 || c->rank > 256 || c->d_pos < 1 ||
+      c->d_pos > 64 || c->d_feat < 1 || c->d_feat > 64 || c->max_L < 1)
+    return BRISK_ERR_SHAPE;
+  if (!aligned16(c->A_h) || !aligned16(c->A_e) || !aligned16(c->P_h) || !aligned16(c->P_e) ||
+      !aligned16(c->W_c) || !aligned2(c->pos_emb) || !aligned2(c->P_phi) || !aligned2(c->W_z) ||
+      !aligned2(c->W_h) || !aligned2(c->W_s) || !aligned2(c->w_g))
+    return BRISK_ERR_UNSUPPORTED;
+  return BRISK_OK;
+}
+
+int rerank_shape_check(const brisk_corrector* c, int32_t B, int32_t L, int32_t K) {
+  if (B < 1 || L < 1 || L > c->max_L || K < 4 || K > 64) return BRISK_ERR_SHAPE;
+  if (static_cast<int64_t>(B) * L > kMaxRows) return BRISK_ERR_SHAPE;
+  return BRISK_OK;
+}
+
+int launch_status() {
+  return hipGetLastError() == hipSuccess ? BRISK_OK : BRISK_ERR_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* brisk_status_str(int status) {
+  switch (status) {
+    case BRISK_OK: return "ok";
+    case BRISK_ERR_NULL: return "a required pointer is NULL";
+    case BRISK_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case BRISK_ERR_UNSUPPORTED: return "unsupported alignment or divisibility (16-byte pointers, d % 8 == 0)";
+    case BRISK_ERR_WORKSPACE: return "workspace missing or too small";
+    case BRISK_ERR_HIP: return "a HIP launch failed";
+    default: return "unknown status";
+  }
+}
+
+int brisk_abi_version(void) { return kAbiVersion; }
+
+int brisk_propose_workspace_size(int32_t rows, int32_t d, int32_t V, int32_t K, size_t* bytes) {
+  if (!bytes) return BRISK_ERR_NULL;
+  if (rows < 1 || rows > kMaxRows || d < 8 || d > kMaxD || K < 1 || K > 64 || V < K)
+    return BRISK_ERR_SHAPE;
+  *bytes = brisk::propose_workspace_bytes(rows, V, K);
+  return BRISK_OK;
+}
+
+int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
+                        int32_t V, int32_t K, float* cand_logit, int32_t* cand_id, void* ws,
+                        size_t ws_bytes, void* stream) {
+  const int st = propose_check(hidden, lm_head, rows, d, V, K, cand_logit, cand_id);
+  if (st != BRISK_OK) return st;
+  const size_t need = brisk::propose_workspace_bytes(rows, V, K);
+  if (ws_bytes < need || (need > 0 && !ws)) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_propose(hidden, lm_head, rows, d, V, K, cand_logit, cand_id, ws,
+                        static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_rerank_workspace_size(const brisk_corrector* c, int32_t B, int32_t L, int32_t K,
+                                size_t* bytes) {
+  if (!bytes || !c) return BRISK_ERR_NULL;
+  if (c->d_state < 1 || c->d_state > 512 || c->d_hproj < 1 || c->d_hproj > 256 ||
+      c->d_tproj < 1 || c->d_tproj > 256 || c->rank < 1 || c->rank > 256)
+    return BRISK_ERR_SHAPE;
+  if (B < 1 || L < 1 || K < 4 || K > 64 || static_cast<int64_t>(B) * L > kMaxRows)
+    return BRISK_ERR_SHAPE;
+  *bytes = brisk::rerank_workspace_bytes(*c, B, L, K);
+  return BRISK_OK;
+}
+
+int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                 const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                 const float* cand_logit, const int32_t* cand_id, int32_t B, int32_t L, int32_t K,
+                 int32_t d, int32_t V, int32_t* selected, float* refined, float* gamma,
+                 float* resid, void* ws, size_t ws_bytes, void* stream) {
+  int st = corrector_check(c);
+  if (st != BRISK_OK) return st;
+  if (!hidden || !ctx_hidden || !anchor_tok || !lm_head || !tok_embed || !cand_logit ||
+      !cand_id || !selected)
+    return BRISK_ERR_NULL;
+  st = rerank_shape_check(c, B, L, K);
+  if (st != BRISK_OK) return st;
+  if (d < 8 || d > kMaxD || V < K) return BRISK_ERR_SHAPE;
+  if (d % 8 != 0 || !aligned16(hidden) || !aligned16(ctx_hidden) || !aligned16(lm_head) ||
+      !aligned16(tok_embed) || !aligned4(anchor_tok) || !aligned4(cand_logit) ||
+      !aligned4(cand_id) || !aligned4(selected) || !aligned4(refined) || !aligned4(gamma) ||
+      !aligned4(resid))
+    return BRISK_ERR_UNSUPPORTED;
+  const size_t need = brisk::rerank_workspace_bytes(*c, B, L, K);
+  if (ws_bytes < need || !ws) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_rerank(*c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
+                       B, L, K, d, V, selected, refined, gamma, resid, ws,
+                       static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,
+                        int32_t* accept_len, int32_t* correction, void* stream) {
+  if (!proposal || !verifier || !accept_len) return BRISK_ERR_NULL;
+  if (B < 1 || L < 1 || static_cast<int64_t>(B) * L > (int64_t{1} << 30)) return BRISK_ERR_SHAPE;
+  if (!aligned4(proposal) || !aligned4(verifier) || !aligned4(accept_len) || !aligned4(correction))
+    return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_verify(proposal, verifier, B, L, accept_len, correction,
+                       static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+}  // extern "C"

@@ -1,0 +1,84 @@
+// Device-side helpers shared by the gfx950 kernels of the decoding hot path.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace brisk {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float floatx4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Low / high bf16 of a packed 32-bit word.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+
+// ---------------------------------------------------------------------------
+// Candidate keys.  A 64-bit key orders (logit descending, id ascending) as a
+// plain unsigned integer: the high word is the float's bits made monotone,
+// the low word is ~id.  The K largest keys are therefore exactly the ordered
+// top-K, independent of the order in which keys are visited.  Key 0 is never
+// produced by a finite logit and marks an empty slot.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t make_key(float logit, uint32_t id) {
+  uint32_t u = __float_as_uint(logit + 0.0f);  // -0 -> +0
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (static_cast<uint64_t>(u) << 32) | static_cast<uint64_t>(0xFFFFFFFFu - id);
+}
+
+__device__ __forceinline__ float key_logit(uint64_t key) {
+  uint32_t u = static_cast<uint32_t>(key >> 32);
+  u = (u & 0x80000000u) ? (u & 0x7FFFFFFFu) : ~u;
+  return __uint_as_float(u);
+}
+
+__device__ __forceinline__ int32_t key_id(uint64_t key) {
+  return static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(key));
+}
+
+// Insert `key` into a list sorted descending, dropping the smallest entry.
+// Branch-free: every slot keeps max(slot, carry) and passes min on.
+template <int N>
+__device__ __forceinline__ void list_insert(uint64_t (&list)[N], uint64_t key) {
+#pragma unroll
+  for (int j = 0; j < N; ++j) {
+    const uint64_t hi = list[j] > key ? list[j] : key;
+    const uint64_t lo = list[j] > key ? key : list[j];
+    list[j] = hi;
+    key = lo;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Wavefront reductions (64 lanes).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off, kWave);
+  return v;
+}
+
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), off, kWave);
+    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), off, kWave);
+    const uint64_t o = (static_cast<uint64_t>(hi) << 32) | lo;
+    v = o > v ? o : v;
+  }
+  return v;
+}
+
+__device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + __expf(-x)); }
+
+__device__ __forceinline__ int clamp_id(int32_t id, int32_t V) {
+  return id < 0 ? 0 : (id >= V ? V - 1 : id);
+}
+
+}  // namespace brisk

@@ -1,0 +1,29 @@
+// Launchers of the gfx950 kernels (host side, internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/brisk.h"
+
+namespace brisk {
+
+// ---- propose: LM head + fused top-K + merge --------------------------------
+size_t propose_workspace_bytes(int rows, int V, int K);
+void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
+                    float* cand_logit, int32_t* cand_id, void* ws, hipStream_t s);
+
+// ---- rerank: hoisted projections + sequential scan -------------------------
+size_t rerank_workspace_bytes(const brisk_corrector& c, int B, int L, int K);
+void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                   const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                   const float* cand_logit, const int32_t* cand_id, int B, int L, int K, int d,
+                   int V, int32_t* selected, float* refined, float* gamma, float* resid, void* ws,
+                   hipStream_t s);
+
+// ---- verify -----------------------------------------------------------------
+void launch_verify(const int32_t* proposal, const int32_t* verifier, int B, int L,
+                   int32_t* accept_len, int32_t* correction, hipStream_t s);
+
+}  // namespace brisk

@@ -1,0 +1,132 @@
+"""Host-side checks of the C ABI that need no GPU.
+
+The library must load and export every function ``include/brisk.h`` declares,
+and every invalid call must be rejected by host validation before any HIP call.
+Each call below is built to fail validation, so none of them launches work.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_33390_amd as brisk
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "brisk.h")
+
+OK, ENULL, ESHAPE, EUNSUP, EWS = 0, -1, -2, -3, -4
+FAKE = 0x10000          # an aligned non-null address that is never dereferenced
+MISALIGNED = 0x10002
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(brisk_\w+)\s*\(", text)))
+
+
+def test_header_declares_the_bound_symbols():
+    assert _declared() == sorted(brisk.ABI_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = brisk.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+
+
+def test_status_strings_and_version():
+    L = brisk.lib()
+    assert L.brisk_abi_version() == 1
+    for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5):
+        assert L.brisk_status_str(st).decode()
+    assert L.brisk_status_str(123).decode() == "unknown status"
+
+
+def _propose(**kw):
+    a = dict(hidden=FAKE, lm_head=FAKE, rows=32, d=4096, V=126464, K=8, cl=FAKE, ci=FAKE,
+             ws=FAKE, ws_bytes=0, stream=None)
+    a.update(kw)
+    return brisk.lib().brisk_propose_block(a["hidden"], a["lm_head"], a["rows"], a["d"], a["V"],
+                                           a["K"], a["cl"], a["ci"], a["ws"], a["ws_bytes"], a["stream"])
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(hidden=None), ENULL), (dict(lm_head=None), ENULL), (dict(cl=None), ENULL),
+    (dict(ci=None), ENULL),
+    (dict(rows=0), ESHAPE), (dict(rows=-3), ESHAPE), (dict(d=0), ESHAPE), (dict(K=0), ESHAPE),
+    (dict(K=65), ESHAPE), (dict(V=4, K=8), ESHAPE), (dict(d=1 << 20), ESHAPE),
+    (dict(d=4100), EUNSUP), (dict(hidden=MISALIGNED), EUNSUP), (dict(lm_head=MISALIGNED), EUNSUP),
+    (dict(ws_bytes=0), EWS), (dict(ws=None, ws_bytes=1 << 40), EWS),
+])
+def test_propose_validation(kw, want):
+    assert _propose(**kw) == want
+
+
+def test_propose_workspace_size_query():
+    n = brisk.propose_workspace_size(32, 4096, 126464, 8)
+    assert n > 0
+    assert _propose(ws_bytes=n - 1) == EWS
+    with pytest.raises(brisk.BriskError):
+        brisk.propose_workspace_size(0, 4096, 126464, 8)
+
+
+def _corr(**kw):
+    dims = dict(d_state=256, d_hproj=128, d_tproj=128, d_pos=32, d_feat=32, rank=128, max_L=32)
+    ptrs = {n: FAKE for n in brisk.PSI_FIELDS}
+    for k, v in kw.items():
+        if k in dims:
+            dims[k] = v
+        else:
+            ptrs[k] = v
+    return brisk._CorrectorC(**dims, **ptrs, alpha=0.0, b_g=0.0)
+
+
+def _rerank(c=None, **kw):
+    a = dict(hidden=FAKE, ctx=FAKE, anchor=FAKE, W=FAKE, E=FAKE, cl=FAKE, ci=FAKE, B=1, L=32, K=8,
+             d=4096, V=126464, sel=FAKE, ref=None, gam=None, res=None, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    c = _corr() if c is None else c
+    return brisk.lib().brisk_rerank(ctypes.byref(c), a["hidden"], a["ctx"], a["anchor"], a["W"], a["E"],
+                                    a["cl"], a["ci"], a["B"], a["L"], a["K"], a["d"], a["V"], a["sel"],
+                                    a["ref"], a["gam"], a["res"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("ckw,kw,want", [
+    (dict(W_c=None), {}, ENULL), (dict(A_h=None), {}, ENULL), ({}, dict(sel=None), ENULL),
+    ({}, dict(anchor=None), ENULL),
+    (dict(d_state=0), {}, ESHAPE), (dict(d_state=513), {}, ESHAPE), (dict(rank=300), {}, ESHAPE),
+    ({}, dict(K=3), ESHAPE), ({}, dict(K=65), ESHAPE), ({}, dict(L=33), ESHAPE), ({}, dict(B=0), ESHAPE),
+    ({}, dict(V=4), ESHAPE),
+    ({}, dict(d=4092), EUNSUP), (dict(W_c=MISALIGNED), {}, EUNSUP), ({}, dict(E=MISALIGNED), EUNSUP),
+    ({}, dict(ws_bytes=16), EWS),
+])
+def test_rerank_validation(ckw, kw, want):
+    assert _rerank(_corr(**ckw), **kw) == want
+
+
+def test_rerank_workspace_size_query():
+    c = _corr()
+    out = ctypes.c_size_t()
+    assert brisk.lib().brisk_rerank_workspace_size(ctypes.byref(c), 64, 32, 8, ctypes.byref(out)) == OK
+    assert out.value > 64 * 32 * 8 * 256 * 4
+    assert brisk.lib().brisk_rerank_workspace_size(ctypes.byref(c), 64, 32, 2, ctypes.byref(out)) == ESHAPE
+
+
+@pytest.mark.parametrize("args,want", [
+    ((None, FAKE, 4, 8, FAKE, None), ENULL), ((FAKE, FAKE, 4, 8, None, None), ENULL),
+    ((FAKE, FAKE, 0, 8, FAKE, None), ESHAPE), ((FAKE, FAKE, 4, 0, FAKE, None), ESHAPE),
+    ((MISALIGNED, FAKE, 4, 8, FAKE, None), EUNSUP),
+])
+def test_verify_validation(args, want):
+    assert brisk.lib().brisk_verify_accept(*args, None) == want
+
+
+def test_python_binding_refuses_host_tensors():
+    import torch
+    h = torch.zeros(4, 64, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="HIP device"):
+        brisk.propose_block(h, h, 4)
+    with pytest.raises(ValueError, match="HIP device"):
+        brisk.verify_accept(torch.zeros(2, 3, dtype=torch.int32), torch.zeros(2, 3, dtype=torch.int32))

@@ -1,0 +1,204 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle.
+
+Every test draws its inputs once with the seeded generator and hands the very
+same tensors to both sides.  Full-size workloads run in the launch
+configuration the benchmark times; there the oracle recomputes a sample of
+rows for the candidate check, and the whole corrector and verification.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+from oracle_io import oracle_inputs
+from parity import SCORE_TOL, check_candidates, check_gpu_order, check_rerank, rerank_pick_ok
+
+pytestmark = pytest.mark.gpu
+
+brisk = pytest.importorskip("paper_2609_33390_amd")
+DEV = "cuda"
+
+
+def _say(*a):
+    print(*a, flush=True)
+
+
+def run_step(blk, *, want_scores=True):
+    wl = blk.wl
+    cl, ci = brisk.propose_block(blk.H, blk.W, wl.K)
+    corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
+    rr = brisk.rerank(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, wl.B, wl.L,
+                      want_scores=want_scores)
+    acc, cor = brisk.verify_accept(rr["selected"], blk.verifier)
+    torch.cuda.synchronize()
+    out = {k: v.cpu().numpy() for k, v in rr.items()}
+    out.update(cand_logit=cl.cpu().numpy(), cand_id=ci.cpu().numpy(), accept=acc.cpu().numpy(),
+               correction=cor.cpu().numpy())
+    return out
+
+
+def sample_rows(rows, n=48, seed=0):
+    if rows <= n:
+        return np.arange(rows)
+    rng = np.random.default_rng(seed)
+    must = {0, rows - 1, min(31, rows - 1), min(32, rows - 1), min(127, rows - 1), min(128, rows - 1)}
+    extra = rng.choice(rows, size=n - len(must), replace=False)
+    return np.array(sorted(must | set(extra.tolist())))
+
+
+def check_step(blk, g, io, rows_sample=None):
+    wl = blk.wl
+    rows = wl.rows
+    rs = np.arange(rows) if rows_sample is None else rows_sample
+    _say(f"  [{wl.name}] oracle logits on {len(rs)} rows")
+    ol = oracle.lm_logits(io["H"][rs], io["W_bits"])
+    check_candidates(g["cand_logit"][rs], g["cand_id"][rs], ol)
+    check_gpu_order(g["cand_logit"], g["cand_id"])
+    _say(f"  [{wl.name}] oracle rerank (GPU candidates, GPU prefix)")
+    orc = oracle.rerank(io["psi"], io["alpha"], io["b_g"], io["H"], io["h_c"], io["x0"], io["W_bits"],
+                        io["E_bits"], g["cand_logit"], g["cand_id"], wl.B, wl.L, prefix=g["selected"])
+    n_near = check_rerank(g, orc)
+    rerank_pick_ok(g["selected"], orc, g["cand_id"])
+    acc, cor = oracle.verify_accept(g["selected"], io["verifier"])
+    assert np.array_equal(acc, g["accept"]) and np.array_equal(cor, g["correction"])
+    return orc, n_near
+
+
+# ------------------------------------------------------------------ tiny, end to end
+def test_tiny_end_to_end():
+    blk = synth.make_block("tiny-d64-v512", "cpu")
+    io = oracle_inputs(blk)
+    g = run_step(_to_dev(blk))
+    check_step(blk, g, io)
+    # unconditioned oracle run: identical tokens and accept length (no near ties here)
+    cl, ci = oracle.propose_block(io["H_bits"], io["W_bits"], blk.wl.K)
+    free = oracle.rerank(io["psi"], io["alpha"], io["b_g"], io["H"], io["h_c"], io["x0"], io["W_bits"],
+                         io["E_bits"], cl, ci, blk.wl.B, blk.wl.L)
+    assert free["margin"].min() > SCORE_TOL
+    assert np.array_equal(free["selected"], g["selected"])
+    acc, _ = oracle.verify_accept(free["selected"], io["verifier"])
+    assert np.array_equal(acc, g["accept"])
+
+
+def _to_dev(blk):
+    """Move a CPU-drawn block to the GPU (same values on both sides)."""
+    import dataclasses
+    t = lambda x: x.to(DEV)
+    return dataclasses.replace(blk, H=t(blk.H), W=t(blk.W), E=t(blk.E), h_c=t(blk.h_c), x0=t(blk.x0),
+                               verifier=t(blk.verifier), targets=t(blk.targets),
+                               psi={k: t(v) for k, v in blk.psi.items()}, sigma=t(blk.sigma))
+
+
+@pytest.mark.parametrize("std", [0.0, 0.3, 1.0])
+def test_tiny_corrector_scales(std):
+    """Zero weights reduce to top-1; larger weights make the corrector change
+    choices, still within tolerance of the oracle."""
+    blk = synth.make_block("tiny-d64-v512", "cpu", psi_std=std, flat_all=std > 0)
+    io = oracle_inputs(blk)
+    g = run_step(_to_dev(blk))
+    check_step(blk, g, io)
+    if std == 0.0:
+        assert np.array_equal(g["selected"].ravel(), g["cand_id"][:, 0])
+        assert np.array_equal(g["refined"], g["cand_logit"])
+        assert np.all(g["resid"] == 0)
+
+
+# ------------------------------------------------------------------ full-size workloads
+FULL = ["llada8b-b1-l32", "llada8b-b64-l32", "dream7b-b16-l32", "llada8b-b256-l16"]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("name", FULL)
+def test_full_workload(name):
+    _say(f"[{name}] generate on GPU")
+    blk = synth.make_block(name, DEV)
+    _say(f"[{name}] run HIP path")
+    g = run_step(blk)
+    io = oracle_inputs(blk)
+    orc, n_near = check_step(blk, g, io, sample_rows(blk.wl.rows))
+    hist = np.bincount(g["accept"], minlength=blk.wl.L + 1)
+    _say(f"[{name}] ok: near-tie rerank rows {n_near}, accept histogram {hist.tolist()}")
+    del blk, io
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.slow
+def test_full_workload_scaled_corrector():
+    """Flat rows with a strong corrector at the 7B wide-vocab shape: the rerank
+    changes choices and still agrees with the oracle."""
+    blk = synth.make_block("dream7b-b16-l32", DEV, psi_std=0.05, flat_all=True)
+    g = run_step(blk)
+    io = oracle_inputs(blk)
+    check_step(blk, g, io, sample_rows(blk.wl.rows, 24))
+    changed = (g["selected"].ravel() != g["cand_id"][:, 0]).mean()
+    _say(f"  corrector changed {changed:.1%} of selections")
+    assert changed > 0.05
+
+
+# ------------------------------------------------------------------ ragged shapes
+RAGGED = [
+    # rows, d, V, K: tails in every tiled dimension
+    (1, 64, 256, 1), (7, 72, 1000, 5), (33, 136, 777, 16), (65, 200, 2049, 8),
+    (130, 64, 4100, 33), (300, 520, 3000, 64), (32, 4096, 513, 4),
+]
+
+
+@pytest.mark.parametrize("rows,d,V,K", RAGGED)
+def test_propose_ragged(rows, d, V, K):
+    g = torch.Generator(device="cpu").manual_seed(rows * 7 + d + V + K)
+    H = torch.randn(rows, d, generator=g).to(torch.bfloat16)
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    cl, ci = brisk.propose_block(H.to(DEV), W.to(DEV), K)
+    torch.cuda.synchronize()
+    Hb, Wb = synth.bf16_bits(H), synth.bf16_bits(W)
+    ol = oracle.lm_logits(oracle.bf16_to_f64(Hb), Wb)
+    check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
+
+
+@pytest.mark.parametrize("B,L,K,d,V,r", [(3, 5, 5, 72, 1000, 32), (2, 9, 4, 136, 600, 96),
+                                          (5, 3, 16, 64, 2000, 320), (70, 2, 8, 64, 512, 256)])
+def test_rerank_ragged(B, L, K, d, V, r):
+    wl = synth.Workload("ragged", B=B, L=L, d=d, V=V, K=K, r=r, sigma=0.3, flat_frac=0.5, seed=B + L + K)
+    blk = synth.make_block(wl, "cpu", psi_std=0.3)
+    io = oracle_inputs(blk)
+    g = run_step(_to_dev(blk))
+    check_step(blk, g, io)
+
+
+def test_duplicate_rows_tie_break():
+    """Bitwise-equal logits (duplicated lm_head rows): the lower id comes first."""
+    blk = synth.make_block("tiny-d64-v512", "cpu", dup_top=True)
+    io = oracle_inputs(blk)
+    g = run_step(_to_dev(blk))
+    ol = oracle.lm_logits(io["H"], io["W_bits"])
+    for r in range(blk.wl.rows):
+        a, b = g["cand_id"][r, :2]
+        if ol[r, a] == ol[r, b]:
+            assert g["cand_logit"][r, 0] == g["cand_logit"][r, 1]
+            assert a < b
+    ties = sum(ol[r, g["cand_id"][r, 0]] == ol[r, g["cand_id"][r, 1]] for r in range(blk.wl.rows))
+    assert ties >= blk.wl.rows // 2
+    check_step(blk, g, io)
+
+
+def test_verify_forced_mismatches_and_long_blocks():
+    rng = np.random.default_rng(1)
+    for L in (1, 8, 63, 64, 65, 100, 200):
+        B = 257
+        ver = rng.integers(0, 1000, size=(B, L)).astype(np.int32)
+        prop = ver.copy()
+        for b in range(B):
+            pos = rng.choice([0, L // 2, L - 1, 63, 64, -1])
+            if 0 <= pos < L:
+                prop[b, pos] += 1
+        acc, cor = brisk.verify_accept(torch.from_numpy(prop).to(DEV), torch.from_numpy(ver).to(DEV))
+        oa, oc = oracle.verify_accept(prop, ver)
+        assert np.array_equal(acc.cpu().numpy(), oa) and np.array_equal(cor.cpu().numpy(), oc)
+
+
+def test_deterministic_repeat():
+    blk = _to_dev(synth.make_block("tiny-d64-v512", "cpu", psi_std=0.5, flat_all=True))
+    a, b = run_step(blk), run_step(blk)
+    for k in a:
+        assert np.array_equal(a[k], b[k]), k
