@@ -22,19 +22,23 @@ namespace {
 // ---------------------------------------------------------------------------
 // gather_proj: out[n, j] = sum_k table[row(n), k] * wt[j, k]   (bf16 in, fp32 out)
 // row(n) = idx[n] (clamped into [0, n_table)) or n when idx is null.
-// MFMA: A = wt rows (M = j), B = gathered rows (N = n).
+// MFMA: A = wt rows (M = j), B = gathered rows (N = n).  The reduction over
+// d is split into `splits` slices (grid z) so that small batches still fill
+// the GPU; slice s writes its partial sums to out + s * n * J and the
+// consumers add the slices in order, which keeps the result deterministic.
 // ---------------------------------------------------------------------------
 struct ProjJob {
   const uint16_t* table;
   const int32_t* idx;
   int n, J, n_table;
   const uint16_t* wt;
-  float* out;  // [n, J]
+  float* out;           // slice s, row n, column j at out[s * slice_stride + n * J + j]
+  size_t slice_stride;  // floats between consecutive slices
 };
 constexpr int kMaxProjJobs = 6;
 struct ProjJobs {
   ProjJob job[kMaxProjJobs];
-  int d;
+  int d, splits;
 };
 
 constexpr int PJ_BN = 64, PJ_BJ = 64, PJ_BK = 64, PJ_STRIDE = PJ_BK + 8;
@@ -47,20 +51,48 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   if (static_cast<int>(blockIdx.x) >= n_jt * n_nt) return;
   const int jt = blockIdx.x % n_jt, nt = blockIdx.x / n_jt;
   const int j0 = jt * PJ_BJ, n0 = nt * PJ_BN;
+  const int chunks = (d + PJ_BK - 1) / PJ_BK;
+  const int per = (chunks + jobs.splits - 1) / jobs.splits;
+  const int c_begin = min(static_cast<int>(blockIdx.z) * per, chunks);
+  const int c_end = min(c_begin + per, chunks);
 
   __shared__ __align__(16) uint16_t sA[PJ_BJ * PJ_STRIDE];
   __shared__ __align__(16) uint16_t sB[PJ_BN * PJ_STRIDE];
-  __shared__ int srow[PJ_BN];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wj = wave & 1, wn = wave >> 1;  // 2 x 2 waves, 32 x 32 each
-  if (tid < PJ_BN) {
-    const int n = n0 + tid;
-    int r = -1;
-    if (n < jb.n) r = jb.idx ? clamp_id(jb.idx[n], jb.n_table) : n;
-    srow[tid] = r;
+
+  // Each thread stages two 16-byte chunks of each operand per step; its
+  // rows are fixed, so the gathered table rows are resolved once.
+  int arow[2], brow[2], col[2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int c = tid + i * 256;
+    const int row = c >> 3;
+    col[i] = (c & 7) * 8;
+    arow[i] = j0 + row < jb.J ? j0 + row : -1;
+    const int n = n0 + row;
+    brow[i] = n < jb.n ? (jb.idx ? clamp_id(jb.idx[n], jb.n_table) : n) : -1;
   }
-  __syncthreads();
+  uint4 ra[2], rb[2];
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int k = k0 + col[i];
+      ra[i] = make_uint4(0, 0, 0, 0);
+      rb[i] = make_uint4(0, 0, 0, 0);
+      if (arow[i] >= 0 && k < d) ra[i] = *reinterpret_cast<const uint4*>(jb.wt + static_cast<size_t>(arow[i]) * d + k);
+      if (brow[i] >= 0 && k < d) rb[i] = *reinterpret_cast<const uint4*>(jb.table + static_cast<size_t>(brow[i]) * d + k);
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int row = (tid + i * 256) >> 3;
+      *reinterpret_cast<uint4*>(sA + row * PJ_STRIDE + col[i]) = ra[i];
+      *reinterpret_cast<uint4*>(sB + row * PJ_STRIDE + col[i]) = rb[i];
+    }
+  };
 
   floatx4 acc[2][2];
 #pragma unroll
@@ -68,39 +100,34 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  for (int k0 = 0; k0 < d; k0 += PJ_BK) {
-    // 64 rows x 64 cols of each operand = 512 16-byte chunks each, 2 per thread.
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = tid + i * 256;
-      const int row = c >> 3, col = (c & 7) * 8;
-      const int k = k0 + col;
-      uint4 va = make_uint4(0, 0, 0, 0), vb = make_uint4(0, 0, 0, 0);
-      const int j = j0 + row;
-      if (j < jb.J && k < d) va = *reinterpret_cast<const uint4*>(jb.wt + static_cast<size_t>(j) * d + k);
-      const int r = srow[row];
-      if (r >= 0 && k < d) vb = *reinterpret_cast<const uint4*>(jb.table + static_cast<size_t>(r) * d + k);
-      *reinterpret_cast<uint4*>(sA + row * PJ_STRIDE + col) = va;
-      *reinterpret_cast<uint4*>(sB + row * PJ_STRIDE + col) = vb;
-    }
+  if (c_begin < c_end) {
+    load(c_begin * PJ_BK);
+    store();
     __syncthreads();
+    for (int ch = c_begin; ch < c_end; ++ch) {
+      const bool more = ch + 1 < c_end;
+      if (more) load((ch + 1) * PJ_BK);
 #pragma unroll
-    for (int kk = 0; kk < PJ_BK; kk += 32) {
-      const int koff = kk + (lane >> 4) * 8;
-      bf16x8 a[2], b[2];
+      for (int kk = 0; kk < PJ_BK; kk += 32) {
+        const int koff = kk + (lane >> 4) * 8;
+        bf16x8 a[2], b[2];
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        a[t] = *reinterpret_cast<const bf16x8*>(sA + (wj * 32 + t * 16 + (lane & 15)) * PJ_STRIDE + koff);
-        b[t] = *reinterpret_cast<const bf16x8*>(sB + (wn * 32 + t * 16 + (lane & 15)) * PJ_STRIDE + koff);
+        for (int t = 0; t < 2; ++t) {
+          a[t] = *reinterpret_cast<const bf16x8*>(sA + (wj * 32 + t * 16 + (lane & 15)) * PJ_STRIDE + koff);
+          b[t] = *reinterpret_cast<const bf16x8*>(sB + (wn * 32 + t * 16 + (lane & 15)) * PJ_STRIDE + koff);
+        }
+#pragma unroll
+        for (int x = 0; x < 2; ++x)
+#pragma unroll
+          for (int y = 0; y < 2; ++y)
+            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
       }
-#pragma unroll
-      for (int x = 0; x < 2; ++x)
-#pragma unroll
-        for (int y = 0; y < 2; ++y)
-          acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
+      __syncthreads();
+      if (more) store();
+      __syncthreads();
     }
-    __syncthreads();
   }
+  float* out = jb.out + static_cast<size_t>(blockIdx.z) * jb.slice_stride;
 #pragma unroll
   for (int x = 0; x < 2; ++x)
 #pragma unroll
@@ -110,7 +137,7 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
       if (n < jb.n) {
 #pragma unroll
         for (int q = 0; q < 4; ++q)
-          if (jb0 + q < jb.J) jb.out[static_cast<size_t>(n) * jb.J + jb0 + q] = acc[x][y][q];
+          if (jb0 + q < jb.J) out[static_cast<size_t>(n) * jb.J + jb0 + q] = acc[x][y][q];
       }
     }
 }
@@ -161,81 +188,198 @@ __global__ __launch_bounds__(256) void cross_dot_kernel(const uint16_t* __restri
 }
 
 // ---------------------------------------------------------------------------
-// lift: out[n, j] = sum_c M(j, c) in[n, c] (+ sum_c M2(j, c) pos[n mod L, c])
-// for j < ds, with M(j, c) = m[j * m_rs + c * m_cs] (bf16) and fp32 inputs.
+// lift: out[n, j] = sum over terms T of sum_c M_T(j, c) in_T(n, c), j < ds.
+// A term reads its input either as fp32 (the projections above) or as bf16
+// (the position table, the feature map P_phi), with arbitrary strides and an
+// optional row period (position index = row mod L); M_T(j, c) =
+// m[j * m_rs + c * m_cs] is a bf16 slice of a corrector matrix.  Tiles of
+// 32 rows x 64 outputs, 2 x 4 outputs per thread; the reduction is staged in
+// LDS 32 columns at a time with the next columns already loading.
 // ---------------------------------------------------------------------------
-struct LiftJob {
-  const float* in;
-  int n, C;
+struct LiftTerm {
+  const void* in;      // fp32 or bf16
+  int in_bf16;
+  int rs, cs, period;  // in(n, c) = in[(period ? n % period : n) * rs + c * cs]
+  int C;
   const uint16_t* m;
   int m_rs, m_cs;
-  const uint16_t* m2;   // nullable: position term
-  const uint16_t* pos;  // [max_L, C2]
-  int C2, L;
-  float* out;           // [n, ds]
 };
-constexpr int kMaxLiftJobs = 5;
+struct LiftJob {
+  LiftTerm t[2];       // second term optional (C = 0)
+  int n;
+  float* out;          // row n -> out + (n / grp) * blk + (n % grp) * ds
+  int grp;
+  size_t blk;
+};
+constexpr int kMaxLiftJobs = 9;
 struct LiftJobs {
   LiftJob job[kMaxLiftJobs];
-  int ds, m2_rs;
+  int ds;
 };
-constexpr int LT_N = 16;
-constexpr int LT_MAXC = 256;
+constexpr int LT_BN = 32, LT_BJ = 64, LT_BC = 32;
+
+__device__ __forceinline__ float lift_in(const LiftTerm& t, int n, int c) {
+  const size_t idx = static_cast<size_t>(t.period ? n % t.period : n) * t.rs + static_cast<size_t>(c) * t.cs;
+  return t.in_bf16 ? bf16_to_f32(static_cast<const uint16_t*>(t.in)[idx]) : static_cast<const float*>(t.in)[idx];
+}
 
 __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
-  const LiftJob& jb = jobs.job[blockIdx.y];
-  const int n0 = blockIdx.x * LT_N;
-  if (n0 >= jb.n) return;
-  __shared__ float s_in[LT_N * LT_MAXC];
+  const LiftJob& jb = jobs.job[blockIdx.z];
+  const int n0 = blockIdx.x * LT_BN, j0 = blockIdx.y * LT_BJ;
+  const int ds = jobs.ds;
+  if (n0 >= jb.n || j0 >= ds) return;
+  __shared__ __align__(16) float s_in[LT_BC][LT_BN + 4];
+  __shared__ __align__(16) float s_m[LT_BC][LT_BJ + 4];
   const int tid = threadIdx.x;
-  for (int e = tid; e < LT_N * jb.C; e += 256) {
-    const int n = n0 + e / jb.C;
-    s_in[e] = n < jb.n ? jb.in[static_cast<size_t>(n) * jb.C + e % jb.C] : 0.f;
-  }
-  __syncthreads();
-  for (int j = tid; j < jobs.ds; j += 256) {
-    float acc[LT_N];
+  const int tn = tid & 15, tj = tid >> 4;
+  const int CA = jb.t[0].C, c_total = CA + jb.t[1].C;
+  float acc[2][4];
 #pragma unroll
-    for (int q = 0; q < LT_N; ++q) acc[q] = 0.f;
-    for (int c = 0; c < jb.C; ++c) {
-      const float mv = bf16_to_f32(jb.m[static_cast<size_t>(j) * jb.m_rs + static_cast<size_t>(c) * jb.m_cs]);
+  for (int x = 0; x < 2; ++x)
 #pragma unroll
-      for (int q = 0; q < LT_N; ++q) acc[q] += mv * s_in[q * jb.C + c];
+    for (int y = 0; y < 4; ++y) acc[x][y] = 0.f;
+
+  float rin[4], rm[8];
+  auto load = [&](int c0) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + q * 256;
+      const int cc = e & (LT_BC - 1), rr = e >> 5;
+      const int c = c0 + cc, n = n0 + rr;
+      float v = 0.f;
+      if (n < jb.n && c < c_total) v = c < CA ? lift_in(jb.t[0], n, c) : lift_in(jb.t[1], n, c - CA);
+      rin[q] = v;
     }
-    if (jb.m2) {
-      for (int c = 0; c < jb.C2; ++c) {
-        const float mv = bf16_to_f32(jb.m2[static_cast<size_t>(j) * jobs.m2_rs + c]);
 #pragma unroll
-        for (int q = 0; q < LT_N; ++q) {
-          const int n = n0 + q;
-          acc[q] += mv * bf16_to_f32(jb.pos[(n % jb.L) * jb.C2 + c]);
-        }
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + q * 256;
+      // walk along whichever index is contiguous in memory (decided by the
+      // first term for the whole tile, so every thread agrees on the mapping)
+      const bool jfast = jb.t[0].m_rs == 1;
+      const int cc = jfast ? (e >> 6) : (e & (LT_BC - 1));
+      const int rr = jfast ? (e & 63) : (e >> 5);
+      const int cx = c0 + cc, j = j0 + rr;
+      float v = 0.f;
+      if (j < ds && cx < c_total) {
+        const LiftTerm& tt = cx < CA ? jb.t[0] : jb.t[1];
+        const int cl = cx < CA ? cx : cx - CA;
+        v = bf16_to_f32(tt.m[static_cast<size_t>(j) * tt.m_rs + static_cast<size_t>(cl) * tt.m_cs]);
       }
+      rm[q] = v;
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + q * 256;
+      s_in[e & (LT_BC - 1)][e >> 5] = rin[q];
     }
 #pragma unroll
-    for (int q = 0; q < LT_N; ++q) {
-      const int n = n0 + q;
-      if (n < jb.n) jb.out[static_cast<size_t>(n) * jobs.ds + j] = acc[q];
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + q * 256;
+      const bool jfast = jb.t[0].m_rs == 1;
+      const int cc = jfast ? (e >> 6) : (e & (LT_BC - 1));
+      const int rr = jfast ? (e & 63) : (e >> 5);
+      s_m[cc][rr] = rm[q];
+    }
+  };
+
+  load(0);
+  store();
+  __syncthreads();
+  for (int c0 = 0; c0 < c_total; c0 += LT_BC) {
+    const bool more = c0 + LT_BC < c_total;
+    if (more) load(c0 + LT_BC);
+#pragma unroll 8
+    for (int cc = 0; cc < LT_BC; ++cc) {
+      const float2 a = *reinterpret_cast<const float2*>(&s_in[cc][tn * 2]);
+      const float4 b = *reinterpret_cast<const float4*>(&s_m[cc][tj * 4]);
+      const float av[2] = {a.x, a.y}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int x = 0; x < 2; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] += av[x] * bv[y];
+    }
+    __syncthreads();
+    if (more) store();
+    __syncthreads();
+  }
+#pragma unroll
+  for (int x = 0; x < 2; ++x) {
+    const int n = n0 + tn * 2 + x;
+    if (n >= jb.n) continue;
+    float* o = jb.out + static_cast<size_t>(n / jb.grp) * jb.blk + static_cast<size_t>(n % jb.grp) * ds;
+#pragma unroll
+    for (int y = 0; y < 4; ++y) {
+      const int j = j0 + tj * 4 + y;
+      if (j < ds) o[j] = acc[x][y];
     }
   }
 }
 
 // ---------------------------------------------------------------------------
-// scan: one wavefront per sequence, the L dependent steps in order.
-// Lane `lane` owns state elements e = lane + 64 j, j < PL.
+// slice_sum: in-place, in-order sum of the split-K slices into slice 0.
+// ---------------------------------------------------------------------------
+struct SliceArr {
+  float* p;
+  size_t n;       // elements per slice (a multiple of 4)
+  size_t stride;  // floats between slices
+};
+constexpr int kMaxSliceArrs = 4, kMaxSplits = 16;
+struct SliceArrs {
+  SliceArr arr[kMaxSliceArrs];
+  int splits;
+};
+
+__global__ __launch_bounds__(256) void slice_sum_kernel(SliceArrs sa) {
+  const SliceArr& A = sa.arr[blockIdx.y];
+  const size_t i = (static_cast<size_t>(blockIdx.x) * 256 + threadIdx.x) * 4;
+  if (i >= A.n) return;
+  float4 v[kMaxSplits];
+#pragma unroll
+  for (int s = 0; s < kMaxSplits; ++s)
+    if (s < sa.splits) v[s] = *reinterpret_cast<const float4*>(A.p + s * A.stride + i);
+  float4 t = v[0];
+#pragma unroll
+  for (int s = 1; s < kMaxSplits; ++s)
+    if (s < sa.splits) {
+      t.x += v[s].x;
+      t.y += v[s].y;
+      t.z += v[s].z;
+      t.w += v[s].w;
+    }
+  *reinterpret_cast<float4*>(A.p + i) = t;
+}
+
+// ---------------------------------------------------------------------------
+// scan: one workgroup per sequence, one 64-wide slice of the state per wave.
+//
+// The lift kernel leaves each row's step inputs in one contiguous "step
+// block" of F = 2 + 3K vectors of length ds: [AZ, AH, EH_0..EH_{K-1},
+// TZ_0..TZ_{K-1}, TH_0..TH_{K-1}] (TZ_k/TH_k: what candidate k of this row
+// feeds into the next step).  A step therefore loads with buffer
+// instructions whose only per-field arithmetic is a scalar offset.
+//
+// The loads for the next D-1 rows are in flight while a step runs: D
+// statically indexed buffers are rotated by unrolling the step loop D times,
+// loads are unconditional (indices clamped, never masked at load time) and
+// outputs are staged in LDS, so the loop holds no stores and the compiler can
+// wait for exactly the buffer a step consumes.
+//
+// Reductions: the K residual dot products and the gate product are summed
+// inside each 16-lane row with DPP (all values interleaved), the row sums of
+// every wave go to LDS, and after one barrier every lane adds the 4 * waves
+// row sums of its value in a fixed order, so all waves take the same decision.
 // ---------------------------------------------------------------------------
 struct ScanArgs {
-  int B, L, K, ds, d_in, feat_off, df;
+  int B, L, K, ds;
   const float* U0;   // [2, B, ds]  A_h h_c, A_e E(x_0)
   const float* X;    // [NC + B]
-  const float* TZ;   // [NC + B, ds]
-  const float* TH;
-  const float* EH;   // [NC, ds]
-  const float* AZ;   // [rows, ds]
-  const float* AH;
-  const uint16_t* W_z;
-  const uint16_t* W_h;
-  const uint16_t* P_phi;
+  const float* SB;   // [rows, F, ds] step blocks
+  const float* TZA;  // [B, ds] anchor-token inputs of step 0
+  const float* THA;
+  const float* FZ;   // [5, ds] W_z[:, feat] P_phi
+  const float* FH;   // [5, ds] W_h[:, feat] P_phi
   const uint16_t* w_g;
   float alpha, b_g;
   const float* cand_logit;
@@ -247,133 +391,255 @@ struct ScanArgs {
   float* resid;
 };
 
-template <int PL>
-__global__ __launch_bounds__(256) void scan_kernel(ScanArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (b >= a.B) return;
+template <int KM>
+struct StepData {
+  float az, ah;
+  float eh[KM];
+  float tz[KM], th[KM];
+  float cl, xs;
+  int ci;
+};
+
+__device__ __forceinline__ float buf_ld(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
+// Loads of step i (row clamped into the block).  Candidates k >= K read a
+// duplicate of candidate K-1 and lanes past ds read element ds-1; consumers
+// ignore those values (k >= K is never selected or used, lanes past ds hold
+// u = 0, lanes >= K are masked where scores are formed).
+template <int KM>
+__device__ __forceinline__ void load_step(StepData<KM>& s, const ScanArgs& a,
+                                          __amdgpu_buffer_rsrc_t rsb, int voff, int b, int i,
+                                          int lane) {
+  const int ii = i < a.L ? i : a.L - 1;
+  const int F = 2 + 3 * a.K;
+  const int vb = a.ds * 4;                // bytes per vector
+  const int base = ii * F * vb;           // this row's step block inside the sequence
+  s.az = buf_ld(rsb, voff, base);
+  s.ah = buf_ld(rsb, voff, base + vb);
+#pragma unroll
+  for (int k = 0; k < KM; ++k) {
+    const int kk = k < a.K ? k : a.K - 1;
+    s.eh[k] = buf_ld(rsb, voff, base + (2 + kk) * vb);
+    s.tz[k] = buf_ld(rsb, voff, base + (2 + a.K + kk) * vb);
+    s.th[k] = buf_ld(rsb, voff, base + (2 + 2 * a.K + kk) * vb);
+  }
+  const size_t nl = (static_cast<size_t>(b) * a.L + ii) * a.K + (lane < a.K ? lane : a.K - 1);
+  s.cl = a.cand_logit[nl];
+  s.xs = a.X[nl];
+  s.ci = a.cand_id[nl];
+}
+
+constexpr int kScanOutChunk = 32;  // steps whose outputs are staged in LDS at once
+constexpr int kScanMaxWaves = 8;
+
+template <int KM, int D>
+__global__ __launch_bounds__(512) void scan_kernel(ScanArgs a) {
+  constexpr int NV = KM + 1;                 // K residual sums + the gate sum
+  constexpr int NQ = kScanMaxWaves * 4;      // row sums per value
+  __shared__ __align__(16) float red[2][NV][NQ];
+  __shared__ float o_ref[kScanOutChunk][KM], o_res[kScanOutChunk][KM], o_gam[kScanOutChunk];
+  __shared__ int o_sel[kScanOutChunk];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int nw = blockDim.x >> 6;
+  const int nq = nw * 4;
+  const int b = blockIdx.x;
   const int ds = a.ds, K = a.K, L = a.L;
   const int NC = a.B * L * K;
+  const int e = w * 64 + lane;
+  const bool ok = e < ds;
+  const int ec = ok ? e : ds - 1;
+  const int F = 2 + 3 * K;
+  const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.SB + static_cast<size_t>(b) * L * F * ds), static_cast<short>(0),
+      L * F * ds * 4, 0x00020000);
+  const int voff = ec * 4;
 
-  float u[PL], wgu[PL], fz[PL][5], fh[PL][5];
+  float fz[5], fh[5];
+  const float u0a = a.U0[static_cast<size_t>(b) * ds + ec];
+  const float u0b = a.U0[static_cast<size_t>(a.B + b) * ds + ec];
+  const float wg_e = bf16_to_f32(a.w_g[ec]);
 #pragma unroll
-  for (int j = 0; j < PL; ++j) {
-    const int e = lane + 64 * j;
-    const bool ok = e < ds;
-    u[j] = ok ? tanhf(a.U0[static_cast<size_t>(b) * ds + e] + a.U0[static_cast<size_t>(a.B + b) * ds + e]) : 0.f;
-    wgu[j] = ok ? bf16_to_f32(a.w_g[e]) : 0.f;
-#pragma unroll
-    for (int f = 0; f < 5; ++f) {
-      float sz = 0.f, sh = 0.f;
-      if (ok) {
-        for (int q = 0; q < a.df; ++q) {
-          const float p = bf16_to_f32(a.P_phi[q * 5 + f]);
-          sz += bf16_to_f32(a.W_z[static_cast<size_t>(e) * a.d_in + a.feat_off + q]) * p;
-          sh += bf16_to_f32(a.W_h[static_cast<size_t>(e) * a.d_in + a.feat_off + q]) * p;
-        }
-      }
-      fz[j][f] = sz;
-      fh[j][f] = sh;
-    }
+  for (int f = 0; f < 5; ++f) {
+    fz[f] = a.FZ[f * ds + ec];
+    fh[f] = a.FH[f * ds + ec];
   }
+  float u = ok ? tanhf(u0a + u0b) : 0.f;
+  const float wgu = ok ? wg_e : 0.f;
   float wgphi[5];
 #pragma unroll
   for (int f = 0; f < 5; ++f) wgphi[f] = bf16_to_f32(a.w_g[ds + f]);
   const float sig_alpha = sigmoidf_(a.alpha);
 
-  int prev_n = NC + b;
+  float prev_tz = a.TZA[static_cast<size_t>(b) * ds + ec];
+  float prev_th = a.THA[static_cast<size_t>(b) * ds + ec];
+  float prev_x = a.X[NC + b];
   int prev_tok = a.anchor[b];
-  for (int i = 0; i < L; ++i) {
-    const int r = b * L + i;
-    const float cl = lane < K ? a.cand_logit[static_cast<size_t>(r) * K + lane] : 0.f;
-    const int ci = lane < K ? a.cand_id[static_cast<size_t>(r) * K + lane] : -1;
-    const float c0 = __shfl(cl, 0), c1 = __shfl(cl, 1), c3 = __shfl(cl, 3);
-    const int id0 = __shfl(ci, 0);
-    const bool in4 = __ballot(lane < 4 && ci == prev_tok) != 0;
+  const int my_v = lane < K ? lane : 0;  // the residual sum this lane assembles
+
+  auto flush = [&](int i0, int n) {
+    __syncthreads();
+    if (w == 0) {
+      for (int t = 0; t < n; ++t) {
+        const size_t r = static_cast<size_t>(b) * L + i0 + t;
+        if (lane < K) {
+          if (a.refined) a.refined[r * K + lane] = o_ref[t][lane];
+          if (a.resid) a.resid[r * K + lane] = o_res[t][lane];
+        }
+        if (lane == 0) {
+          a.selected[r] = o_sel[t];
+          if (a.gamma) a.gamma[r] = o_gam[t];
+        }
+      }
+    }
+    __syncthreads();
+  };
+
+  auto step = [&](const StepData<KM>& c, int i) {
+    const float c0 = readlane_f32(c.cl, 0), c1 = readlane_f32(c.cl, 1), c3 = readlane_f32(c.cl, 3);
+    const int id0 = __builtin_amdgcn_readlane(c.ci, 0);
+    const bool in4 = __ballot(lane < 4 && c.ci == prev_tok) != 0;
     float phi[5];
     phi[0] = c0 - c1;
     phi[1] = c0 - c3;
     phi[2] = prev_tok == id0 ? 1.f : 0.f;
     phi[3] = in4 ? 1.f : 0.f;
-    phi[4] = c0 - a.X[prev_n];
+    phi[4] = c0 - prev_x;
 
-    float gs = 0.f;
+    float gz = c.az + prev_tz, gh = c.ah + prev_th;
 #pragma unroll
-    for (int j = 0; j < PL; ++j) {
-      const int e = lane + 64 * j;
-      if (e < ds) {
-        float gz = a.AZ[static_cast<size_t>(r) * ds + e] + a.TZ[static_cast<size_t>(prev_n) * ds + e];
-        float gh = a.AH[static_cast<size_t>(r) * ds + e] + a.TH[static_cast<size_t>(prev_n) * ds + e];
-#pragma unroll
-        for (int f = 0; f < 5; ++f) {
-          gz += fz[j][f] * phi[f];
-          gh += fh[j][f] * phi[f];
-        }
-        const float z = sigmoidf_(gz);
-        u[j] = (1.f - z) * u[j] + z * gh;
-        gs += u[j] * wgu[j];
-      }
+    for (int f = 0; f < 5; ++f) {
+      gz += fz[f] * phi[f];
+      gh += fh[f] * phi[f];
     }
-    float s = wave_sum(gs) + a.b_g;
+    const float z = sigmoidf_(gz);
+    u = ok ? (1.f - z) * u + z * gh : 0.f;
+
+    float v[NV];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) v[k] = u * c.eh[k];
+    v[KM] = u * wgu;
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] += dpp_f32<0xB1>(v[k]);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] += dpp_f32<0x4E>(v[k]);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] += dpp_f32<0x141>(v[k]);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) v[k] += dpp_f32<0x140>(v[k]);
+    const int buf = i & 1;
+    if ((lane & 15) == 0) {
+      const int q = w * 4 + (lane >> 4);
+#pragma unroll
+      for (int k = 0; k < NV; ++k) red[buf][k][q] = v[k];
+    }
+    __syncthreads();
+    float my_d = 0.f, s = 0.f;
+    for (int q = 0; q < nq; q += 4) {
+      const float4 rd = *reinterpret_cast<const float4*>(&red[buf][my_v][q]);
+      const float4 rg = *reinterpret_cast<const float4*>(&red[buf][KM][q]);
+      my_d += (rd.x + rd.y) + (rd.z + rd.w);
+      s += (rg.x + rg.y) + (rg.z + rg.w);
+    }
+    s += a.b_g;
 #pragma unroll
     for (int f = 0; f < 5; ++f) s += wgphi[f] * phi[f];
     const float g = sig_alpha * sigmoidf_(s);
-
-    float my_d = 0.f;
-    for (int k = 0; k < K; ++k) {
-      const float* eh = a.EH + (static_cast<size_t>(r) * K + k) * ds;
-      float p = 0.f;
-#pragma unroll
-      for (int j = 0; j < PL; ++j) {
-        const int e = lane + 64 * j;
-        if (e < ds) p += u[j] * eh[e];
+    my_d = lane < K ? my_d : 0.f;
+    const float lt = c.cl + g * my_d;
+    const float m = wave_allmax(lane < K ? lt : -INFINITY);
+    const uint64_t hit = __ballot(lane < K && lt == m);
+    const int kstar = hit ? __builtin_ctzll(hit) : 0;
+    const int sel = __builtin_amdgcn_readlane(c.ci, kstar);
+    const int t = i % kScanOutChunk;
+    if (w == 0) {
+      if (lane < K) {
+        o_ref[t][lane] = lt;
+        o_res[t][lane] = my_d;
       }
-      p = wave_sum(p);
-      if (lane == k) my_d = p;
+      if (lane == 0) {
+        o_sel[t] = sel;
+        o_gam[t] = g;
+      }
     }
-    const float lt = cl + g * my_d;
-    const uint64_t key = lane < K ? make_key(lt, static_cast<uint32_t>(lane)) : 0ull;
-    const int kstar = key_id(wave_max_u64(key));
-    const int sel = __shfl(ci, kstar);
-    if (lane < K) {
-      if (a.refined) a.refined[static_cast<size_t>(r) * K + lane] = lt;
-      if (a.resid) a.resid[static_cast<size_t>(r) * K + lane] = my_d;
+    float tz = c.tz[0], th = c.th[0];
+#pragma unroll
+    for (int k = 1; k < KM; ++k) {
+      tz = k == kstar ? c.tz[k] : tz;
+      th = k == kstar ? c.th[k] : th;
     }
-    if (lane == 0) {
-      a.selected[r] = sel;
-      if (a.gamma) a.gamma[r] = g;
-    }
-    prev_n = r * K + kstar;
+    prev_tz = tz;
+    prev_th = th;
+    prev_x = readlane_f32(c.xs, kstar);
     prev_tok = sel;
+    if (t == kScanOutChunk - 1 || i == L - 1) flush(i - t, t + 1);
+  };
+
+  StepData<KM> q[D];
+#pragma unroll
+  for (int t = 0; t < D; ++t) load_step<KM>(q[t], a, rsb, voff, b, t, lane);
+  for (int i = 0; i < L; i += D) {
+#pragma unroll
+    for (int t = 0; t < D; ++t) {
+      if (i + t < L) step(q[t], i + t);
+      load_step<KM>(q[t], a, rsb, voff, b, i + t + D, lane);
+    }
   }
 }
 
 struct Layout {
-  size_t PE, PC, PH, U0, X, TZ, TH, EH, AZ, AH, total;
+  size_t PE, PC, PH, U0, X, SB, TZA, THA, FZ, FH, total;
+  size_t sPE, sPC, sPH, sU0;  // floats between split-K slices (multiples of 64)
+  int splits;
 };
+
+int proj_tiles(int n, int J) { return ((J + PJ_BJ - 1) / PJ_BJ) * ((n + PJ_BN - 1) / PJ_BN); }
+
+// Split the gather projections' reduction so that about 1024 workgroups run
+// even when the batch is small; never more than 16 slices.
+int proj_splits(const brisk_corrector& c, int B, int L, int K) {
+  const int rows = B * L, NC = rows * K;
+  const int tiles = proj_tiles(NC, c.d_tproj) + proj_tiles(B, c.d_tproj) + proj_tiles(NC, c.rank) +
+                    proj_tiles(rows, c.d_hproj) + 2 * proj_tiles(B, c.d_state);
+  int sp = 1024 / (tiles > 0 ? tiles : 1);
+  return sp < 1 ? 1 : (sp > 16 ? 16 : sp);
+}
 
 Layout rerank_layout(const brisk_corrector& c, int B, int L, int K) {
   const size_t rows = static_cast<size_t>(B) * L, NC = rows * K, NP = NC + B;
   const size_t ds = c.d_state;
   Layout l{};
+  l.splits = proj_splits(c, B, L, K);
+  const size_t S = l.splits;
+  auto pad = [](size_t n) { return (n + 63) / 64 * 64; };
+  l.sPE = pad(NP * c.d_tproj);
+  l.sPC = pad(NC * c.rank);
+  l.sPH = pad(rows * c.d_hproj);
+  l.sU0 = pad(2 * static_cast<size_t>(B) * ds);
   size_t off = 0;
   auto take = [&](size_t floats) {
     const size_t o = off;
     off += (floats * sizeof(float) + 255) / 256 * 256;
     return o;
   };
-  l.PE = take(NP * c.d_tproj);
-  l.PC = take(NC * c.rank);
-  l.PH = take(rows * c.d_hproj);
-  l.U0 = take(2 * static_cast<size_t>(B) * ds);
+  l.PE = take(S * l.sPE);
+  l.PC = take(S * l.sPC);
+  l.PH = take(S * l.sPH);
+  l.U0 = take(S * l.sU0);
   l.X = take(NP);
-  l.TZ = take(NP * ds);
-  l.TH = take(NP * ds);
-  l.EH = take(NC * ds);
-  l.AZ = take(rows * ds);
-  l.AH = take(rows * ds);
+  l.SB = take(rows * (2 + 3 * static_cast<size_t>(K)) * ds);
+  l.TZA = take(static_cast<size_t>(B) * ds);
+  l.THA = take(static_cast<size_t>(B) * ds);
+  l.FZ = take(5 * ds);
+  l.FH = take(5 * ds);
   l.total = off;
   return l;
+}
+
+template <int KM, int D>
+void launch_scan(const ScanArgs& sa, int B, int nw, hipStream_t s) {
+  hipLaunchKernelGGL((scan_kernel<KM, D>), dim3(B), dim3(64 * nw), 0, s, sa);
 }
 
 }  // namespace
@@ -394,48 +660,82 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   const int ds = c.d_state;
   const int d_in = c.d_hproj + c.d_tproj + c.d_pos + c.d_feat;
   const int tp_off = c.d_hproj, pos_off = c.d_hproj + c.d_tproj, feat_off = pos_off + c.d_pos;
+  const int S = lay.splits;
 
+  // Slices of PE are [NP, d_tproj]: candidate rows, then anchor rows.
+  // Slices of U0 are [2, B, ds]: A_h h_c, then A_e E(x_0).
+  const size_t sPE = lay.sPE, sPC = lay.sPC, sPH = lay.sPH, sU0 = lay.sU0;
   ProjJobs pj{};
   pj.d = d;
-  pj.job[0] = ProjJob{tok_embed, cand_id, NC, c.d_tproj, V, c.P_e, F(lay.PE)};
-  pj.job[1] = ProjJob{tok_embed, anchor_tok, B, c.d_tproj, V, c.P_e, F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj};
-  pj.job[2] = ProjJob{lm_head, cand_id, NC, c.rank, V, c.W_c, F(lay.PC)};
-  pj.job[3] = ProjJob{hidden, nullptr, rows, c.d_hproj, rows, c.P_h, F(lay.PH)};
-  pj.job[4] = ProjJob{ctx_hidden, nullptr, B, ds, B, c.A_h, F(lay.U0)};
-  pj.job[5] = ProjJob{tok_embed, anchor_tok, B, ds, V, c.A_e, F(lay.U0) + static_cast<size_t>(B) * ds};
+  pj.splits = S;
+  pj.job[0] = ProjJob{tok_embed, cand_id, NC, c.d_tproj, V, c.P_e, F(lay.PE), sPE};
+  pj.job[1] = ProjJob{tok_embed, anchor_tok, B, c.d_tproj, V, c.P_e, F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj, sPE};
+  pj.job[2] = ProjJob{lm_head, cand_id, NC, c.rank, V, c.W_c, F(lay.PC), sPC};
+  pj.job[3] = ProjJob{hidden, nullptr, rows, c.d_hproj, rows, c.P_h, F(lay.PH), sPH};
+  pj.job[4] = ProjJob{ctx_hidden, nullptr, B, ds, B, c.A_h, F(lay.U0), sU0};
+  pj.job[5] = ProjJob{tok_embed, anchor_tok, B, ds, V, c.A_e, F(lay.U0) + static_cast<size_t>(B) * ds, sU0};
   int max_tiles = 0;
   for (int j = 0; j < kMaxProjJobs; ++j) {
-    const int t = ((pj.job[j].J + PJ_BJ - 1) / PJ_BJ) * ((pj.job[j].n + PJ_BN - 1) / PJ_BN);
+    const int t = proj_tiles(pj.job[j].n, pj.job[j].J);
     max_tiles = t > max_tiles ? t : max_tiles;
   }
-  hipLaunchKernelGGL(gather_proj_kernel, dim3(max_tiles, kMaxProjJobs), dim3(256), 0, s, pj);
+  hipLaunchKernelGGL(gather_proj_kernel, dim3(max_tiles, kMaxProjJobs, S), dim3(256), 0, s, pj);
 
   hipLaunchKernelGGL(cross_dot_kernel, dim3((NP + 3) / 4), dim3(256), 0, s, lm_head, hidden, cand_id,
                      anchor_tok, B, L, K, d, V, F(lay.X));
 
+  if (S > 1) {
+    SliceArrs sl{};
+    sl.splits = S;
+    sl.arr[0] = SliceArr{F(lay.PE), sPE, sPE};
+    sl.arr[1] = SliceArr{F(lay.PC), sPC, sPC};
+    sl.arr[2] = SliceArr{F(lay.PH), sPH, sPH};
+    sl.arr[3] = SliceArr{F(lay.U0), sU0, sU0};
+    size_t mx = sPE > sPC ? sPE : sPC;
+    mx = mx > sPH ? mx : sPH;
+    mx = mx > sU0 ? mx : sU0;
+    const int blocks = static_cast<int>((mx / 4 + 255) / 256);
+    hipLaunchKernelGGL(slice_sum_kernel, dim3(blocks, kMaxSliceArrs), dim3(256), 0, s, sl);
+  }
+
+  // Step blocks: row r holds F = 2 + 3K vectors [AZ, AH, EH_k, TZ_k, TH_k].
+  const int FB = 2 + 3 * K;
+  const size_t blk = static_cast<size_t>(FB) * ds;
+  float* SB = F(lay.SB);
   LiftJobs lj{};
   lj.ds = ds;
-  lj.m2_rs = d_in;
-  lj.job[0] = LiftJob{F(lay.PE), NP, c.d_tproj, c.W_z + tp_off, d_in, 1, nullptr, nullptr, 0, L, F(lay.TZ)};
-  lj.job[1] = LiftJob{F(lay.PE), NP, c.d_tproj, c.W_h + tp_off, d_in, 1, nullptr, nullptr, 0, L, F(lay.TH)};
-  lj.job[2] = LiftJob{F(lay.PC), NC, c.rank, c.W_s, 1, ds, nullptr, nullptr, 0, L, F(lay.EH)};
-  lj.job[3] = LiftJob{F(lay.PH), rows, c.d_hproj, c.W_z, d_in, 1, c.W_z + pos_off, c.pos_emb, c.d_pos, L, F(lay.AZ)};
-  lj.job[4] = LiftJob{F(lay.PH), rows, c.d_hproj, c.W_h, d_in, 1, c.W_h + pos_off, c.pos_emb, c.d_pos, L, F(lay.AH)};
-  hipLaunchKernelGGL(lift_kernel, dim3((NP + LT_N - 1) / LT_N, kMaxLiftJobs), dim3(256), 0, s, lj);
+  const float* PEa = F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj;
+  auto fterm = [](const float* in, int C, const uint16_t* m, int m_rs, int m_cs) {
+    return LiftTerm{in, 0, C, 1, 0, C, m, m_rs, m_cs};
+  };
+  const LiftTerm none{nullptr, 0, 0, 0, 0, 0, nullptr, 0, 0};
+  const LiftTerm posz{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1};
+  const LiftTerm posh{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1};
+  const size_t vds = static_cast<size_t>(ds);
+  lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, NC, SB + (2 + K) * vds, K, blk};
+  lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, NC, SB + (2 + 2 * K) * vds, K, blk};
+  lj.job[2] = LiftJob{{fterm(F(lay.PC), c.rank, c.W_s, 1, ds), none}, NC, SB + 2 * vds, K, blk};
+  lj.job[3] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_z, d_in, 1), posz}, rows, SB, 1, blk};
+  lj.job[4] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_h, d_in, 1), posh}, rows, SB + vds, 1, blk};
+  lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, B, F(lay.TZA), 1, vds};
+  lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, B, F(lay.THA), 1, vds};
+  // feature maps W_z[:, feat] P_phi and W_h[:, feat] P_phi as [5, ds]: input row f is column f of P_phi
+  lj.job[7] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1}, none}, 5, F(lay.FZ), 1, vds};
+  lj.job[8] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1}, none}, 5, F(lay.FH), 1, vds};
+  hipLaunchKernelGGL(lift_kernel, dim3((NC + LT_BN - 1) / LT_BN, (ds + LT_BJ - 1) / LT_BJ, kMaxLiftJobs),
+                     dim3(256), 0, s, lj);
 
   ScanArgs sa{};
-  sa.B = B; sa.L = L; sa.K = K; sa.ds = ds; sa.d_in = d_in; sa.feat_off = feat_off; sa.df = c.d_feat;
-  sa.U0 = F(lay.U0); sa.X = F(lay.X); sa.TZ = F(lay.TZ); sa.TH = F(lay.TH); sa.EH = F(lay.EH);
-  sa.AZ = F(lay.AZ); sa.AH = F(lay.AH);
-  sa.W_z = c.W_z; sa.W_h = c.W_h; sa.P_phi = c.P_phi; sa.w_g = c.w_g;
+  sa.B = B; sa.L = L; sa.K = K; sa.ds = ds;
+  sa.U0 = F(lay.U0); sa.X = F(lay.X); sa.SB = SB; sa.TZA = F(lay.TZA); sa.THA = F(lay.THA);
+  sa.FZ = F(lay.FZ); sa.FH = F(lay.FH); sa.w_g = c.w_g;
   sa.alpha = c.alpha; sa.b_g = c.b_g;
   sa.cand_logit = cand_logit; sa.cand_id = cand_id; sa.anchor = anchor_tok;
   sa.selected = selected; sa.refined = refined; sa.gamma = gamma; sa.resid = resid;
-  const dim3 grid((B + 3) / 4), block(256);
-  if (ds <= 64) hipLaunchKernelGGL(scan_kernel<1>, grid, block, 0, s, sa);
-  else if (ds <= 128) hipLaunchKernelGGL(scan_kernel<2>, grid, block, 0, s, sa);
-  else if (ds <= 256) hipLaunchKernelGGL(scan_kernel<4>, grid, block, 0, s, sa);
-  else hipLaunchKernelGGL(scan_kernel<8>, grid, block, 0, s, sa);
+  const int nw = (ds + 63) / 64;
+  if (K <= 8) launch_scan<8, 4>(sa, B, nw, s);
+  else if (K <= 16) launch_scan<16, 3>(sa, B, nw, s);
+  else launch_scan<64, 1>(sa, B, nw, s);
 }
 
 }  // namespace brisk

@@ -49,6 +49,10 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return (bid % NXCD) * per + bid / NXCD;
 }
 
+// Whether the per-position lists fit in the kernel's LDS for the in-workgroup merge.
+template <class C, int KP>
+constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 <= C::LDS_BYTES;
+
 template <class C, int KP>
 __global__ __launch_bounds__(C::NT) void lmhead_topk_kernel(
     const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int rows, int d, int V,
@@ -179,44 +183,92 @@ __global__ __launch_bounds__(C::NT) void lmhead_topk_kernel(
     }
   }
 
+  // Merge the TPP lists of each position inside the workgroup (pairwise
+  // tree through LDS) so one list per (row, vocabulary group) leaves the
+  // kernel.  Lists are stored [slot][thread] so neighbouring threads touch
+  // neighbouring words.
   const int r = r0 + ep;
-  if (r < rows) {
-    uint64_t* dst =
-        partial + (static_cast<size_t>(r) * n_parts + static_cast<size_t>(group) * C::TPP + esub) * KP;
+  if constexpr (kWgMerge<C, KP>) {
+    uint64_t* sk = reinterpret_cast<uint64_t*>(smem);
+    __syncthreads();
 #pragma unroll
-    for (int j = 0; j < KP; ++j) dst[j] = list[j];
+    for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
+    __syncthreads();
+#pragma unroll
+    for (int s = C::TPP / 2; s >= 1; s >>= 1) {
+      if (esub < s) {
+        const int other = (esub + s) * C::BR + ep;
+#pragma unroll
+        for (int j = 0; j < KP; ++j) {
+          const uint64_t key = sk[j * C::NT + other];
+          if (key > list[KP - 1]) list_insert(list, key);
+        }
+#pragma unroll
+        for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
+      }
+      __syncthreads();
+    }
+    if (esub == 0 && r < rows) {
+      uint64_t* dst = partial + (static_cast<size_t>(r) * n_parts + group) * KP;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) dst[j] = list[j];
+    }
+  } else {
+    if (r < rows) {
+      uint64_t* dst =
+          partial + (static_cast<size_t>(r) * n_parts + static_cast<size_t>(group) * C::TPP + esub) * KP;
+#pragma unroll
+      for (int j = 0; j < KP; ++j) dst[j] = list[j];
+    }
   }
 }
 
-// One wavefront per row: each lane folds a strided share of the row's partial
-// keys into a private list, then the wave pops the K largest heads in order.
+// One workgroup per row: every thread folds a strided share of the row's
+// partial keys into a private list, then the lists are merged pairwise through
+// LDS; thread 0's list is the row's ordered top-KP.
 template <int KP>
 __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restrict__ partial,
                                                          int rows, int n_keys, int K,
                                                          float* __restrict__ cand_logit,
                                                          int32_t* __restrict__ cand_id) {
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (row >= rows) return;
+  constexpr int NT = 256, BATCH = 4;
+  __shared__ uint64_t sk[KP * NT];
+  const int tid = threadIdx.x;
+  const int row = blockIdx.x;
   const uint64_t* src = partial + static_cast<size_t>(row) * n_keys;
   uint64_t list[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
-  for (int i = lane; i < n_keys; i += 64) {
-    const uint64_t key = src[i];
-    if (key > list[KP - 1]) list_insert(list, key);
-  }
-  for (int k = 0; k < K; ++k) {
-    const uint64_t best = wave_max_u64(list[0]);
-    if (list[0] == best) {  // keys are unique per row: exactly one lane pops
+  for (int i0 = tid; i0 < n_keys; i0 += NT * BATCH) {
+    uint64_t kb[BATCH];
 #pragma unroll
-      for (int j = 0; j < KP - 1; ++j) list[j] = list[j + 1];
-      list[KP - 1] = 0;
+    for (int q = 0; q < BATCH; ++q) {
+      const int i = i0 + q * NT;
+      kb[q] = i < n_keys ? src[i] : 0ull;
     }
-    if (lane == 0) {
-      cand_logit[static_cast<size_t>(row) * K + k] = key_logit(best);
-      cand_id[static_cast<size_t>(row) * K + k] = key_id(best);
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q)
+      if (kb[q] > list[KP - 1]) list_insert(list, kb[q]);
+  }
+#pragma unroll
+  for (int j = 0; j < KP; ++j) sk[j * NT + tid] = list[j];
+  __syncthreads();
+  for (int s = NT / 2; s >= 1; s >>= 1) {
+    if (tid < s) {
+#pragma unroll
+      for (int j = 0; j < KP; ++j) {
+        const uint64_t key = sk[j * NT + tid + s];
+        if (key > list[KP - 1]) list_insert(list, key);
+      }
+#pragma unroll
+      for (int j = 0; j < KP; ++j) sk[j * NT + tid] = list[j];
     }
+    __syncthreads();
+  }
+  if (tid < K) {
+    const uint64_t key = sk[tid * NT];
+    cand_logit[static_cast<size_t>(row) * K + tid] = key_logit(key);
+    cand_id[static_cast<size_t>(row) * K + tid] = key_id(key);
   }
 }
 
@@ -241,8 +293,13 @@ Plan make_plan_for(int cfg, int rows, int V, int K) {
   p.n_vtiles = (V + C::BV - 1) / C::BV;
   p.tiles_per_group = 1;
   p.n_groups = (p.n_vtiles + p.tiles_per_group - 1) / p.tiles_per_group;
-  p.n_parts = p.n_groups * C::TPP;
   p.KP = K <= 4 ? 4 : K <= 8 ? 8 : K <= 16 ? 16 : K <= 32 ? 32 : 64;
+  const bool wg_merge = p.KP == 4    ? kWgMerge<C, 4>
+                        : p.KP == 8  ? kWgMerge<C, 8>
+                        : p.KP == 16 ? kWgMerge<C, 16>
+                        : p.KP == 32 ? kWgMerge<C, 32>
+                                     : kWgMerge<C, 64>;
+  p.n_parts = p.n_groups * (wg_merge ? 1 : C::TPP);
   return p;
 }
 
@@ -268,7 +325,7 @@ void launch_kp(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, in
     case 1: launch_tile<MidRows, KP>(p, H, W, rows, d, V, partial, s); break;
     default: launch_tile<LargeRows, KP>(p, H, W, rows, d, V, partial, s); break;
   }
-  hipLaunchKernelGGL((topk_merge_kernel<KP>), dim3((rows + 3) / 4), dim3(256), 0, s, partial, rows,
+  hipLaunchKernelGGL((topk_merge_kernel<KP>), dim3(rows), dim3(256), 0, s, partial, rows,
                      p.n_parts * KP, K, cand_logit, cand_id);
 }
 
