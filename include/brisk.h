@@ -111,7 +111,8 @@ int brisk_propose_workspace_size(int32_t rows, int32_t d, int32_t V, int32_t K, 
  *   cand_id     [rows, K]  int32  out: candidate token ids
  *   ws          device scratch of at least brisk_propose_workspace_size bytes
  *
- * Limits: 1 <= rows, 8 <= d <= 65536, 1 <= K <= 64, K <= V <= 2^31 - 1.
+ * Limits: 1 <= rows <= 2^20, 8 <= d <= 65536, 1 <= K <= 64, K <= V; V*d*2 and
+ * rows*d*2 below 2^32 bytes (BRISK_ERR_UNSUPPORTED otherwise).
  */
 int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head,
                         int32_t rows, int32_t d, int32_t V, int32_t K,
@@ -141,7 +142,8 @@ int brisk_rerank_workspace_size(const brisk_corrector* c, int32_t B, int32_t L, 
  *   gamma       [B*L]    fp32   out, nullable: gate gamma_i
  *   resid       [B*L, K] fp32   out, nullable: residual <W_s u_i, W_c E_out(v)>
  *
- * Limits: 4 <= K <= 64 (the features read the top-4), 1 <= L <= max_L.
+ * Limits: 4 <= K <= 64 (the features read the top-4), 1 <= L <= max_L,
+ * B*L <= 2^20, L*(2+3K)*d_state*4 below 2^31 bytes.
  */
 int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
                  const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,

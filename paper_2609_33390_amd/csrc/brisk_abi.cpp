@@ -26,6 +26,10 @@ int propose_check(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows,
   if (d % 8 != 0 || !aligned16(hidden) || !aligned16(lm_head) || !aligned4(cand_logit) ||
       !aligned4(cand_id))
     return BRISK_ERR_UNSUPPORTED;
+  // the LM-head kernel addresses both matrices with 32-bit byte offsets
+  if (static_cast<uint64_t>(V) * d * 2 >= (uint64_t{1} << 32) ||
+      static_cast<uint64_t>(rows) * d * 2 >= (uint64_t{1} << 32))
+    return BRISK_ERR_UNSUPPORTED;
   return BRISK_OK;
 }
 
@@ -119,6 +123,9 @@ int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_
   st = rerank_shape_check(c, B, L, K);
   if (st != BRISK_OK) return st;
   if (d < 8 || d > kMaxD || V < K) return BRISK_ERR_SHAPE;
+  // the scan addresses one sequence's step vectors with 32-bit byte offsets
+  if (static_cast<uint64_t>(L) * (2 + 3 * static_cast<uint64_t>(K)) * c->d_state * 4 >= (uint64_t{1} << 31))
+    return BRISK_ERR_UNSUPPORTED;
   if (d % 8 != 0 || !aligned16(hidden) || !aligned16(ctx_hidden) || !aligned16(lm_head) ||
       !aligned16(tok_embed) || !aligned4(anchor_tok) || !aligned4(cand_logit) ||
       !aligned4(cand_id) || !aligned4(selected) || !aligned4(refined) || !aligned4(gamma) ||

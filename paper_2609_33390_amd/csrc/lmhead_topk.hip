@@ -3,10 +3,21 @@
 // Proposal logits l[r, v] = <hidden[r], lm_head[v]> (Section 3.3, Algorithm
 // 1(b) first step) are produced tile by tile on bf16 MFMA with fp32
 // accumulation and consumed in the same kernel: every tile is folded into
-// per-(row, slice) top-K lists of 64-bit keys, so the [rows, V] logits are
-// never written.  A second kernel merges the lists of one row into the
-// ordered candidate set C_i = TopK(q_i, K) (Section 3.3; Appendix head
+// per-(row, vocabulary group) top-K lists of 64-bit keys, so the [rows, V]
+// logits are never written.  A second kernel merges the lists of one row into
+// the ordered candidate set C_i = TopK(q_i, K) (Section 3.3; Appendix head
 // details): logit descending, token id ascending among equal logits.
+//
+// Pipeline.  Each workgroup owns one row tile and a contiguous group of
+// vocabulary tiles, and streams the reduction slices of all its tiles as one
+// continuous sequence of stages: global memory is copied straight into LDS
+// (global_load_lds, no staging registers), STAGES slices deep, so the loads
+// of the next tile's first slices are already in flight while the current
+// tile's top-K epilogue runs.  Each thread waits only for its own copies of
+// the slice about to be read (an explicit vmcnt that leaves the younger
+// slices in flight) and then meets the workgroup at a barrier.  Staged rows
+// are dense with their 16-byte chunks XOR-swizzled, which keeps the MFMA
+// operand reads (16 lanes, 16 rows, one chunk) free of bank conflicts.
 #include "device_common.h"
 #include "kernels.h"
 
@@ -14,33 +25,52 @@ namespace brisk {
 
 namespace {
 
-constexpr int BK = 64;                // reduction slice staged per step
-constexpr int LDS_STRIDE = BK + 8;    // bf16 per staged row: 144 B breaks bank aliasing
-
-// Tile geometry.  The vocabulary runs along the MFMA M dimension (A = lm_head
-// rows) and the block positions along N (B = hidden rows), so one lane's four
-// accumulator values are four consecutive vocabulary ids of one position.
-template <int BV_, int BR_, int WAVES_V_, int WAVES_R_, int EPI_V_>
+template <int BV_, int BR_, int WAVES_V_, int WAVES_R_, int BK_, int STAGES_>
 struct TileCfg {
-  static constexpr int BV = BV_, BR = BR_, WAVES_V = WAVES_V_, WAVES_R = WAVES_R_;
-  static constexpr int EPI_V = EPI_V_;
-  static constexpr int NT = 64 * WAVES_V * WAVES_R;
-  static constexpr int WV = BV / WAVES_V, WR = BR / WAVES_R;
-  static constexpr int TV = WV / 16, TR = WR / 16;
-  static constexpr int TPP = NT / BR;  // epilogue threads per position
-  static constexpr int STAGE_BYTES = (BV + BR) * LDS_STRIDE * 2;
-  static constexpr int EPI_BYTES = BR * (EPI_V + 1) * 4;
-  static constexpr int LDS_BYTES = STAGE_BYTES > EPI_BYTES ? STAGE_BYTES : EPI_BYTES;
-  static constexpr int W_CHUNKS = BV * BK / 8, H_CHUNKS = BR * BK / 8;
-  static constexpr int W_PER_T = (W_CHUNKS + NT - 1) / NT, H_PER_T = (H_CHUNKS + NT - 1) / NT;
+  static constexpr int BV = BV_, BR = BR_, WAVES_V = WAVES_V_, WAVES_R = WAVES_R_, BK = BK_;
+  static constexpr int STAGES = STAGES_;
+  // the epilogue stages one 16-column accumulator block of every wave at a time
+  static constexpr int EPI_V = 16 * WAVES_V;
+  static constexpr int NW = WAVES_V * WAVES_R, NT = 64 * NW;
+  static constexpr int WV = BV / WAVES_V, WR = BR / WAVES_R, TV = WV / 16, TR = WR / 16;
+  static constexpr int CPR = BK / 8;            // 16-byte chunks per staged row
+  static constexpr int RPI = 64 / CPR;          // staged rows one DMA instruction fills
+  static constexpr int ROWS = BV + BR;          // staged rows per stage: lm_head tile, then hidden tile
+  static constexpr int NDMA = ROWS / RPI / NW;  // DMA instructions per wave per stage
+  static constexpr int STAGE_BYTES = ROWS * BK * 2;
+  static constexpr int TPP = NT / BR;           // epilogue threads per position
+  static constexpr int EPI_STRIDE = EPI_V + 4;  // floats per staged logit row
+  static constexpr int EPI_BYTES = BR * EPI_STRIDE * 4;
+  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES + EPI_BYTES;
+  static_assert(ROWS % (RPI * NW) == 0 && BV % RPI == 0, "DMA instructions must tile the stage");
   static_assert(WV % 16 == 0 && WR % 16 == 0, "wave tile must be a multiple of 16");
-  static_assert(NT % BR == 0, "threads must cover the positions evenly");
-  static_assert(BV % EPI_V == 0 && WV % 16 == 0, "epilogue chunking");
+  static_assert(NT % BR == 0 && (TPP & (TPP - 1)) == 0, "epilogue thread mapping");
+  static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8), "reduction slice");
+  static_assert(EPI_V % (4 * TPP) == 0, "epilogue chunking");
+  static_assert((STAGES - 2) * NDMA <= 63, "vmcnt range");
+  static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
 
+// 16-byte slot that holds chunk c of staged row r (an involution in c).
+template <int CPR>
+__device__ __forceinline__ int swz(int r, int c) {
+  return c ^ ((r / (16 / CPR)) & (CPR - 1));
+}
+
+// Wait until at most N vector-memory operations of this thread are
+// outstanding and all its LDS operations are done, then barrier.
+template <int N>
+__device__ __forceinline__ void stage_sync() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4) | (0 << 8));
+  asm volatile("s_barrier" ::: "memory");
+}
+__device__ __forceinline__ void lds_sync() { stage_sync<63>(); }
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
 // XCD-aware block order.  Consecutive workgroup ids are dealt round-robin to
-// the 8 XCDs; remapping gives each XCD a contiguous range of logical tiles so
-// the row tiles that share one lm_head tile run on the same L2.
+// the 8 XCDs; remapping gives each XCD a contiguous range of logical ids so
+// the row tiles that share lm_head tiles run on the same L2.
 __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   constexpr int NXCD = 8;
   const int per = nblocks / NXCD;
@@ -49,151 +79,163 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return (bid % NXCD) * per + bid / NXCD;
 }
 
-// Whether the per-position lists fit in the kernel's LDS for the in-workgroup merge.
+// Whether the per-position lists fit in LDS for the in-workgroup merge (the
+// stage buffers are idle by then).
 template <class C, int KP>
 constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 <= C::LDS_BYTES;
 
 template <class C, int KP>
 __global__ __launch_bounds__(C::NT) void lmhead_topk_kernel(
     const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int rows, int d, int V,
-    int n_rtiles, int n_vtiles, int tiles_per_group, uint64_t* __restrict__ partial,
-    int n_parts) {
+    int n_rtiles, int n_vtiles, int tiles_per_group, uint64_t* __restrict__ partial, int n_parts) {
   __shared__ __align__(16) unsigned char smem[C::LDS_BYTES];
-  uint16_t* sW = reinterpret_cast<uint16_t*>(smem);
-  uint16_t* sH = sW + C::BV * LDS_STRIDE;
-  float* sL = reinterpret_cast<float*>(smem);
+  float* sE = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  // the wave index is uniform per wave; saying so keeps LDS bases in scalars
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave % C::WAVES_V, wr = wave / C::WAVES_V;
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int rt = logical % n_rtiles;         // row tile fastest: row tiles of one
-  const int group = logical / n_rtiles;      // vocabulary group run side by side
+  const int rt = logical % n_rtiles;
+  const int group = logical / n_rtiles;
   const int r0 = rt * C::BR;
+  const int vt_begin = group * tiles_per_group;
+  const int n_tiles = min(tiles_per_group, n_vtiles - vt_begin);
+  const int nk = (d + C::BK - 1) / C::BK;
+  const int tail = (d % C::BK) / 8;  // valid chunks of the last slice (0: slice is full)
+
+  // ---- copy issue: stage g = (tile g / nk, slice g % nk); past the end the
+  // last slice is re-read so every wave issues the same number of copies.
+  // Buffer resources bound-check every copy: lm_head rows >= V and hidden
+  // rows >= rows read as zeros.  Byte offsets fit in 32 bits (checked on the
+  // host).
+  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(W), static_cast<short>(0), static_cast<int>(static_cast<unsigned>(V) * d * 2u), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(H), static_cast<short>(0), static_cast<int>(static_cast<unsigned>(rows) * d * 2u), 0x00020000);
+  const unsigned row_bytes = static_cast<unsigned>(d) * 2u;
+  // lane part of a copy's byte offset: row lane / CPR of the instruction's rows,
+  // the chunk its slot holds (the swizzle phase depends on the parity of the
+  // instruction's first row block when CPR = 8)
+  unsigned lane_voff[2];
+#pragma unroll
+  for (int par = 0; par < 2; ++par) {
+    const int R = par * C::RPI + lane / C::CPR;
+    lane_voff[par] = static_cast<unsigned>(lane / C::CPR) * row_bytes +
+                     static_cast<unsigned>(swz<C::CPR>(R, lane % C::CPR)) * 16u;
+  }
+  auto issue = [&](int g) {
+    int tl = g / nk, kt = g % nk;
+    if (tl >= n_tiles) {
+      tl = n_tiles - 1;
+      kt = nk - 1;
+    }
+    const unsigned v0 = static_cast<unsigned>((vt_begin + tl) * C::BV), k0b = static_cast<unsigned>(kt * C::BK) * 2u;
+    unsigned char* base = smem + (g % C::STAGES) * C::STAGE_BYTES;
+#pragma unroll
+    for (int i = 0; i < C::NDMA; ++i) {
+      const int j = i * C::NW + wave;
+      const unsigned lv = lane_voff[C::CPR == 8 ? (j & 1) : 0];
+      if (j * C::RPI < C::BV) {
+        const unsigned off = lv + (v0 + static_cast<unsigned>(j * C::RPI)) * row_bytes + k0b;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(base + j * 1024), 16, off, 0, 0, 0);
+      } else {
+        const unsigned off = lv + static_cast<unsigned>(r0 + j * C::RPI - C::BV) * row_bytes + k0b;
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rh, (lds_ptr_t)(base + j * 1024), 16, off, 0, 0, 0);
+      }
+    }
+  };
+
+  // per-lane parts of the MFMA operand addresses (see swz: independent of the 16-row block)
+  const int l15 = lane & 15;
+  int lane_off[C::BK / 32];
+#pragma unroll
+  for (int kk = 0; kk < C::BK / 32; ++kk)
+    lane_off[kk] = (l15 * C::CPR + ((kk * 4 + (lane >> 4)) ^ (l15 / (16 / C::CPR)))) * 16;
 
   const int ep = tid % C::BR, esub = tid / C::BR;
   uint64_t list[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
 
-  const int vt_begin = group * tiles_per_group;
-  const int vt_end = min(vt_begin + tiles_per_group, n_vtiles);
-  for (int vt = vt_begin; vt < vt_end; ++vt) {
-    const int v0 = vt * C::BV;
-    floatx4 acc[C::TV][C::TR];
+  floatx4 acc[C::TV][C::TR];
 #pragma unroll
-    for (int a = 0; a < C::TV; ++a)
+  for (int a = 0; a < C::TV; ++a)
 #pragma unroll
-      for (int b = 0; b < C::TR; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int b = 0; b < C::TR; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    uint4 rw[C::W_PER_T], rh[C::H_PER_T];
-    auto load = [&](int k0) {
 #pragma unroll
-      for (int i = 0; i < C::W_PER_T; ++i) {
-        const int c = tid + i * C::NT;
-        const int row = c / (BK / 8), col = (c % (BK / 8)) * 8;
-        const int v = v0 + row, k = k0 + col;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (c < C::W_CHUNKS && v < V && k < d)
-          val = *reinterpret_cast<const uint4*>(W + static_cast<size_t>(v) * d + k);
-        rw[i] = val;
-      }
-#pragma unroll
-      for (int i = 0; i < C::H_PER_T; ++i) {
-        const int c = tid + i * C::NT;
-        const int row = c / (BK / 8), col = (c % (BK / 8)) * 8;
-        const int r = r0 + row, k = k0 + col;
-        uint4 val = make_uint4(0, 0, 0, 0);
-        if (c < C::H_CHUNKS && r < rows && k < d)
-          val = *reinterpret_cast<const uint4*>(H + static_cast<size_t>(r) * d + k);
-        rh[i] = val;
-      }
-    };
-    auto store = [&]() {
-#pragma unroll
-      for (int i = 0; i < C::W_PER_T; ++i) {
-        const int c = tid + i * C::NT;
-        if (c < C::W_CHUNKS)
-          *reinterpret_cast<uint4*>(sW + (c / (BK / 8)) * LDS_STRIDE + (c % (BK / 8)) * 8) = rw[i];
-      }
-#pragma unroll
-      for (int i = 0; i < C::H_PER_T; ++i) {
-        const int c = tid + i * C::NT;
-        if (c < C::H_CHUNKS)
-          *reinterpret_cast<uint4*>(sH + (c / (BK / 8)) * LDS_STRIDE + (c % (BK / 8)) * 8) = rh[i];
-      }
-    };
+  for (int st = 0; st < C::STAGES - 1; ++st) issue(st);
 
-    load(0);
-    __syncthreads();  // LDS readers of the previous tile's epilogue are done
-    store();
-    __syncthreads();
-    for (int k0 = 0; k0 < d; k0 += BK) {
-      const bool more = k0 + BK < d;
-      if (more) load(k0 + BK);
+  for (int tl = 0; tl < n_tiles; ++tl) {
+    for (int kt = 0; kt < nk; ++kt) {
+      const int g = tl * nk + kt;
+      stage_sync<(C::STAGES - 2) * C::NDMA>();  // slice g landed; everyone is done with slice g-1
+      issue(g + C::STAGES - 1);                  // refills the buffer slice g-1 used
+      const unsigned char* sb = smem + (g % C::STAGES) * C::STAGE_BYTES;
+      if (tail && kt == nk - 1) {
+        // chunks past d hold re-read data: zero them in the lm_head tile
+        unsigned char* wb = smem + (g % C::STAGES) * C::STAGE_BYTES;
+        const int nz = C::CPR - tail;
+        for (int idx = tid; idx < C::BV * nz; idx += C::NT) {
+          const int R = idx / nz, c = tail + idx % nz;
+          *reinterpret_cast<uint4*>(wb + (R * C::CPR + swz<C::CPR>(R, c)) * 16) = make_uint4(0, 0, 0, 0);
+        }
+        lds_sync();
+      }
 #pragma unroll
-      for (int kk = 0; kk < BK; kk += 32) {
-        bf16x8 a[C::TV], b[C::TR];
-        const int koff = kk + (lane >> 4) * 8;
+      for (int kk = 0; kk < C::BK / 32; ++kk) {
+        bf16x8 b[C::TR];
 #pragma unroll
-        for (int t = 0; t < C::TV; ++t)
-          a[t] = *reinterpret_cast<const bf16x8*>(
-              sW + (wv * C::WV + t * 16 + (lane & 15)) * LDS_STRIDE + koff);
+        for (int y = 0; y < C::TR; ++y)
+          b[y] = *reinterpret_cast<const bf16x8*>(sb + (C::BV + wr * C::WR + y * 16) * C::CPR * 16 + lane_off[kk]);
 #pragma unroll
-        for (int t = 0; t < C::TR; ++t)
-          b[t] = *reinterpret_cast<const bf16x8*>(
-              sH + (wr * C::WR + t * 16 + (lane & 15)) * LDS_STRIDE + koff);
-#pragma unroll
-        for (int x = 0; x < C::TV; ++x)
+        for (int x = 0; x < C::TV; ++x) {
+          const bf16x8 a = *reinterpret_cast<const bf16x8*>(sb + (wv * C::WV + x * 16) * C::CPR * 16 + lane_off[kk]);
 #pragma unroll
           for (int y = 0; y < C::TR; ++y)
-            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
+            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[y], acc[x][y], 0, 0, 0);
+        }
       }
-      __syncthreads();
-      if (more) store();
-      __syncthreads();
     }
 
-    // Fused top-K: stage EPI_V vocabulary columns of the tile at a time as
-    // fp32 [position][column] in LDS; every thread folds the columns of its
-    // position into its running list.
+    // Fused top-K over this tile.  Chunk x stages accumulator block x of
+    // every wave as fp32 [position][wave_v * 16 + column]; each thread then
+    // folds its position's columns into its running list.
+    const int v0 = (vt_begin + tl) * C::BV;
 #pragma unroll
-    for (int c0 = 0; c0 < C::BV; c0 += C::EPI_V) {
+    for (int x = 0; x < C::TV; ++x) {
 #pragma unroll
-      for (int x = 0; x < C::TV; ++x) {
-        const int vbase = wv * C::WV + x * 16;
-        if (vbase >= c0 && vbase < c0 + C::EPI_V) {
+      for (int y = 0; y < C::TR; ++y) {
+        const int p = wr * C::WR + y * 16 + l15;
+        *reinterpret_cast<floatx4*>(sE + p * C::EPI_STRIDE + wv * 16 + (lane >> 4) * 4) = acc[x][y];
+        acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+      }
+      lds_sync();
 #pragma unroll
-          for (int y = 0; y < C::TR; ++y) {
-            const int p = wr * C::WR + y * 16 + (lane & 15);
-            const int vl = vbase - c0 + (lane >> 4) * 4;
+      for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) {
+        const floatx4 v = *reinterpret_cast<const floatx4*>(sE + ep * C::EPI_STRIDE + col);
+        const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);
 #pragma unroll
-            for (int q = 0; q < 4; ++q) sL[p * (C::EPI_V + 1) + vl + q] = acc[x][y][q];
-          }
+        for (int q = 0; q < 4; ++q) {
+          const int vid = vid0 + q;
+          const uint64_t key = make_key(v[q], static_cast<uint32_t>(vid));
+          if (vid < V && key > list[KP - 1]) list_insert(list, key);
         }
       }
-      __syncthreads();
-      for (int col = esub; col < C::EPI_V; col += C::TPP) {
-        const int v = v0 + c0 + col;
-        if (v < V) {
-          const uint64_t key = make_key(sL[ep * (C::EPI_V + 1) + col], static_cast<uint32_t>(v));
-          if (key > list[KP - 1]) list_insert(list, key);
-        }
-      }
-      __syncthreads();
+      lds_sync();
     }
   }
+  stage_sync<0>();  // the trailing copies have landed; LDS is free
 
   // Merge the TPP lists of each position inside the workgroup (pairwise
-  // tree through LDS) so one list per (row, vocabulary group) leaves the
-  // kernel.  Lists are stored [slot][thread] so neighbouring threads touch
-  // neighbouring words.
+  // tree through LDS) so one list per (row, vocabulary group) leaves.
   const int r = r0 + ep;
   if constexpr (kWgMerge<C, KP>) {
     uint64_t* sk = reinterpret_cast<uint64_t*>(smem);
-    __syncthreads();
 #pragma unroll
     for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
-    __syncthreads();
+    lds_sync();
 #pragma unroll
     for (int s = C::TPP / 2; s >= 1; s >>= 1) {
       if (esub < s) {
@@ -206,7 +248,7 @@ __global__ __launch_bounds__(C::NT) void lmhead_topk_kernel(
 #pragma unroll
         for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
       }
-      __syncthreads();
+      lds_sync();
     }
     if (esub == 0 && r < rows) {
       uint64_t* dst = partial + (static_cast<size_t>(r) * n_parts + group) * KP;
@@ -272,13 +314,14 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   }
 }
 
-using SmallRows = TileCfg<256, 32, 4, 1, 256>;   // <= 32 rows: weight streaming
-using MidRows = TileCfg<256, 64, 4, 1, 128>;     // <= 64 rows
-using LargeRows = TileCfg<256, 128, 2, 2, 64>;   // many rows: MFMA bound
+using SmallRows = TileCfg<256, 32, 4, 1, 64, 3>;    // <= 32 rows: weight streaming
+using MidRows = TileCfg<256, 64, 4, 1, 64, 3>;      // <= 64 rows
+using LargeRows = TileCfg<256, 256, 2, 2, 32, 3>;   // many rows: MFMA bound
+
+constexpr int kTargetWorkgroups = 256;  // one persistent workgroup per compute unit
 
 struct Plan {
-  int cfg;        // 0 small, 1 mid, 2 large
-  int BV, BR, TPP;
+  int cfg;  // 0 small, 1 mid, 2 large
   int n_rtiles, n_vtiles, tiles_per_group, n_groups, n_parts, KP;
 };
 
@@ -286,12 +329,11 @@ template <class C>
 Plan make_plan_for(int cfg, int rows, int V, int K) {
   Plan p{};
   p.cfg = cfg;
-  p.BV = C::BV;
-  p.BR = C::BR;
-  p.TPP = C::TPP;
   p.n_rtiles = (rows + C::BR - 1) / C::BR;
   p.n_vtiles = (V + C::BV - 1) / C::BV;
-  p.tiles_per_group = 1;
+  int want = kTargetWorkgroups / p.n_rtiles;
+  want = want < 1 ? 1 : (want > p.n_vtiles ? p.n_vtiles : want);
+  p.tiles_per_group = (p.n_vtiles + want - 1) / want;
   p.n_groups = (p.n_vtiles + p.tiles_per_group - 1) / p.tiles_per_group;
   p.KP = K <= 4 ? 4 : K <= 8 ? 8 : K <= 16 ? 16 : K <= 32 ? 32 : 64;
   const bool wg_merge = p.KP == 4    ? kWgMerge<C, 4>
