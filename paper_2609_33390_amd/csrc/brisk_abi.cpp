@@ -5,7 +5,7 @@
 
 #include <cstdint>
 
-#include "../../include/brisk.h"
+#include "brisk.h"
 #include "kernels.h"
 
 namespace {

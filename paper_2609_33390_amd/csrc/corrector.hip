@@ -207,9 +207,9 @@ struct LiftTerm {
 struct LiftJob {
   LiftTerm t[2];       // second term optional (C = 0)
   int n;
-  float* out;          // row n -> out + (n / grp) * blk + (n % grp) * ds
+  float* out;          // row n -> out + (n / grp) * blk + (n % grp) * vs
   int grp;
-  size_t blk;
+  size_t blk, vs;
 };
 constexpr int kMaxLiftJobs = 9;
 struct LiftJobs {
@@ -308,7 +308,7 @@ __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
   for (int x = 0; x < 2; ++x) {
     const int n = n0 + tn * 2 + x;
     if (n >= jb.n) continue;
-    float* o = jb.out + static_cast<size_t>(n / jb.grp) * jb.blk + static_cast<size_t>(n % jb.grp) * ds;
+    float* o = jb.out + static_cast<size_t>(n / jb.grp) * jb.blk + static_cast<size_t>(n % jb.grp) * jb.vs;
 #pragma unroll
     for (int y = 0; y < 4; ++y) {
       const int j = j0 + tj * 4 + y;
@@ -372,7 +372,7 @@ __global__ __launch_bounds__(256) void slice_sum_kernel(SliceArrs sa) {
 // row sums of its value in a fixed order, so all waves take the same decision.
 // ---------------------------------------------------------------------------
 struct ScanArgs {
-  int B, L, K, ds;
+  int B, L, K, ds, vs;  // vs: floats between the vectors of a step block (>= ds)
   const float* U0;   // [2, B, ds]  A_h h_c, A_e E(x_0)
   const float* X;    // [NC + B]
   const float* SB;   // [rows, F, ds] step blocks
@@ -389,6 +389,7 @@ struct ScanArgs {
   float* refined;
   float* gamma;
   float* resid;
+  float* dump;       // [B, 64] sink for output lanes with nothing to write
 };
 
 template <int KM>
@@ -414,7 +415,7 @@ __device__ __forceinline__ void load_step(StepData<KM>& s, const ScanArgs& a,
                                           int lane) {
   const int ii = i < a.L ? i : a.L - 1;
   const int F = 2 + 3 * a.K;
-  const int vb = a.ds * 4;                // bytes per vector
+  const int vb = a.vs * 4;                // bytes per vector
   const int base = ii * F * vb;           // this row's step block inside the sequence
   s.az = buf_ld(rsb, voff, base);
   s.ah = buf_ld(rsb, voff, base + vb);
@@ -452,8 +453,8 @@ __global__ __launch_bounds__(512) void scan_kernel(ScanArgs a) {
   const int ec = ok ? e : ds - 1;
   const int F = 2 + 3 * K;
   const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(a.SB + static_cast<size_t>(b) * L * F * ds), static_cast<short>(0),
-      L * F * ds * 4, 0x00020000);
+      const_cast<float*>(a.SB + static_cast<size_t>(b) * L * F * a.vs), static_cast<short>(0),
+      L * F * a.vs * 4, 0x00020000);
   const int voff = ec * 4;
 
   float fz[5], fh[5];
@@ -588,8 +589,261 @@ __global__ __launch_bounds__(512) void scan_kernel(ScanArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// scan_lds: the whole sequence in one wavefront (d_state <= 256; lane l holds
+// state elements 4l..4l+3).  The step data of the next rows are copied into
+// an LDS ring straight from global memory - one buffer DMA instruction per
+// 1 KiB vector, and 64-word vectors for the candidate scores, ids and cross
+// logits - and the wave waits only for the row it is about to use.  After
+// the argmax, only the selected candidate's previous-token vectors are read
+// back.  Reductions: DPP inside each 16-lane row, then the four row sums meet
+// in LDS (a single wave needs no barrier for that).
+// ---------------------------------------------------------------------------
+template <int KM>
+struct LdsStage {
+  static constexpr int NVEC = 2 + 3 * KM;       // AZ, AH, EH_k, TZ_k, TH_k
+  static constexpr int NDMA = NVEC + 3;         // + candidate logits, ids, cross logits
+  static constexpr int FLOATS = NVEC * 256 + 3 * 64;
+};
+
+template <int N>
+__device__ __forceinline__ void wait_vm_lgkm0() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4) | (0 << 8));
+}
+
+typedef __attribute__((address_space(3))) void* lds_vptr_t;
+
+// LDS reads of the copy ring, issued as inline assembly.  For an ordinary
+// LDS read the compiler cannot tell the ring slot apart from the slots still
+// being filled by copies and waits for every outstanding copy first, which
+// would undo the prefetch.  The reads here are followed by one explicit
+// lgkmcnt(0) wait; each value then passes through an empty asm ordered after
+// that wait, so no use can be scheduled before the data has arrived.
+typedef float f4_t __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ unsigned lds_addr(const float* p) {
+  return static_cast<unsigned>(reinterpret_cast<size_t>((const __attribute__((address_space(3))) float*)(p)));
+}
+__device__ __forceinline__ f4_t lds_rd128(unsigned addr) {
+  f4_t r;
+  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+__device__ __forceinline__ float lds_rd32(unsigned addr) {
+  float r;
+  asm volatile("ds_read_b32 %0, %1" : "=v"(r) : "v"(addr));
+  return r;
+}
+__device__ __forceinline__ void lds_drain() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+template <class T>
+__device__ __forceinline__ void after_drain(T& x) { asm volatile("" : "+v"(x)); }
+
+template <int KM, int D>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void scan_lds_kernel(ScanArgs a) {
+  using S = LdsStage<KM>;
+  // Each row issues NDMA copies and one output store; waiting for row i
+  // leaves the copies of rows i+1..i+D-2 and the stores of rows i-D+1..i-1
+  // (issued after row i's copies) outstanding.
+  constexpr int kAfter = (D - 2) * S::NDMA + (D - 1);
+  static_assert(kAfter <= 63, "vmcnt range");
+  static_assert(2 * KM <= 62, "output lanes");
+  __shared__ __align__(16) float ring[D * S::FLOATS];
+  const int lane = threadIdx.x;
+  const int b = blockIdx.x;
+  const int ds = a.ds, K = a.K, L = a.L;
+  const int NC = a.B * L * K;
+  const int F = 2 + 3 * K;
+
+  bool okj[4];
+  int ej[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    okj[j] = 4 * lane + j < ds;
+    ej[j] = okj[j] ? 4 * lane + j : ds - 1;
+  }
+  float u[4], wgu[4], fz[4][5], fh[4][5], ptz[4], pth[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const float u0a = a.U0[static_cast<size_t>(b) * ds + ej[j]];
+    const float u0b = a.U0[static_cast<size_t>(a.B + b) * ds + ej[j]];
+    u[j] = okj[j] ? tanhf(u0a + u0b) : 0.f;
+    wgu[j] = okj[j] ? bf16_to_f32(a.w_g[ej[j]]) : 0.f;
+    const float tz = a.TZA[static_cast<size_t>(b) * ds + ej[j]], th = a.THA[static_cast<size_t>(b) * ds + ej[j]];
+    ptz[j] = okj[j] ? tz : 0.f;
+    pth[j] = okj[j] ? th : 0.f;
+#pragma unroll
+    for (int f = 0; f < 5; ++f) {
+      const float z = a.FZ[f * ds + ej[j]], h = a.FH[f * ds + ej[j]];
+      fz[j][f] = okj[j] ? z : 0.f;
+      fh[j][f] = okj[j] ? h : 0.f;
+    }
+  }
+  float wgphi[5];
+#pragma unroll
+  for (int f = 0; f < 5; ++f) wgphi[f] = bf16_to_f32(a.w_g[ds + f]);
+  const float sig_alpha = sigmoidf_(a.alpha);
+  float prev_x = a.X[NC + b];
+  int prev_tok = a.anchor[b];
+  // materialise the set-up values here (the compiler would otherwise sink
+  // their loads into the loop), then start counting copies from an empty queue
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    asm volatile("" : "+v"(u[j]), "+v"(wgu[j]), "+v"(ptz[j]), "+v"(pth[j]));
+#pragma unroll
+    for (int f = 0; f < 5; ++f) asm volatile("" : "+v"(fz[j][f]), "+v"(fh[j][f]));
+  }
+  asm volatile("" : "+v"(prev_x), "+v"(prev_tok));
+  wait_vm_lgkm0<0>();
+
+  const size_t row0 = static_cast<size_t>(b) * L;
+  const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.SB + row0 * F * 256), static_cast<short>(0), L * F * 1024, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rcl = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.cand_logit + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rci = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int32_t*>(a.cand_id + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rxs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.X + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+
+  // Copies of row i (clamped to the block) into ring slot i % D.  Candidate
+  // slots k >= K repeat candidate K-1 so every row issues exactly NDMA copies.
+  auto issue = [&](int i) {
+    const int ii = i < L ? i : L - 1;
+    float* st = ring + (i % D) * S::FLOATS;
+    const unsigned rb = static_cast<unsigned>(ii * F) * 1024u;
+#pragma unroll
+    for (int v = 0; v < S::NVEC; ++v) {
+      int f;
+      if (v < 2) f = v;
+      else if (v < 2 + KM) f = 2 + min(v - 2, K - 1);
+      else if (v < 2 + 2 * KM) f = 2 + K + min(v - 2 - KM, K - 1);
+      else f = 2 + 2 * K + min(v - 2 - 2 * KM, K - 1);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_vptr_t)(st + v * 256), 16, lane * 16,
+                                               rb + static_cast<unsigned>(f) * 1024u, 0, 0);
+    }
+    const unsigned cb = static_cast<unsigned>(ii * K) * 4u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rcl, (lds_vptr_t)(st + S::NVEC * 256), 4, lane * 4, cb, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rci, (lds_vptr_t)(st + S::NVEC * 256 + 64), 4, lane * 4, cb, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_vptr_t)(st + S::NVEC * 256 + 128), 4, lane * 4, cb, 0, 0);
+  };
+
+  // where this lane writes its output of a row (see the store below)
+  float* const dump = a.dump + static_cast<size_t>(b) * 64 + lane;
+  auto out_ptr = [&](size_t r) -> float* {
+    if (lane < K) return a.refined ? a.refined + r * K + lane : dump;
+    if (lane < 2 * K) return a.resid ? a.resid + r * K + (lane - K) : dump;
+    if (lane == 62) return a.gamma ? a.gamma + r : dump;
+    if (lane == 63) return reinterpret_cast<float*>(a.selected + r);
+    return dump;
+  };
+
+  // Prologue: the first D-1 rows, each followed by a store to the sink so the
+  // queue already has the steady-state shape (copies of a row, then one store).
+#pragma unroll
+  for (int t = 0; t < D - 1; ++t) {
+    issue(t);
+    *dump = 0.f;
+  }
+  for (int i = 0; i < L; ++i) {
+    wait_vm_lgkm0<kAfter>();  // row i has landed; reads of slot (i-1) % D are done
+    issue(i + D - 1);
+    const float* st = ring + (i % D) * S::FLOATS;
+    const unsigned sv = lds_addr(st) + 16u * lane, sw = lds_addr(st) + 4u * lane;
+    f4_t az = lds_rd128(sv), ah = lds_rd128(sv + 1024u);
+    f4_t eh[KM];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) eh[k] = lds_rd128(sv + (2u + k) * 1024u);
+    float cl = lds_rd32(sw + S::NVEC * 1024u);
+    float cif = lds_rd32(sw + S::NVEC * 1024u + 256u);
+    float xs = lds_rd32(sw + S::NVEC * 1024u + 512u);
+    lds_drain();
+    after_drain(az);
+    after_drain(ah);
+#pragma unroll
+    for (int k = 0; k < KM; ++k) after_drain(eh[k]);
+    after_drain(cl);
+    after_drain(cif);
+    after_drain(xs);
+    const int ci = __float_as_int(cif);
+
+    const float c0 = readlane_f32(cl, 0), c1 = readlane_f32(cl, 1), c3 = readlane_f32(cl, 3);
+    const int id0 = __builtin_amdgcn_readlane(ci, 0);
+    const bool in4 = __ballot(lane < 4 && ci == prev_tok) != 0;
+    float phi[5];
+    phi[0] = c0 - c1;
+    phi[1] = c0 - c3;
+    phi[2] = prev_tok == id0 ? 1.f : 0.f;
+    phi[3] = in4 ? 1.f : 0.f;
+    phi[4] = c0 - prev_x;
+
+    const float azv[4] = {az.x, az.y, az.z, az.w}, ahv[4] = {ah.x, ah.y, ah.z, ah.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float gz = azv[j] + ptz[j], gh = ahv[j] + pth[j];
+#pragma unroll
+      for (int f = 0; f < 5; ++f) {
+        gz += fz[j][f] * phi[f];
+        gh += fh[j][f] * phi[f];
+      }
+      const float z = sigmoidf_(gz);
+      u[j] = okj[j] ? (1.f - z) * u[j] + z * gh : 0.f;
+    }
+
+    float v[KM + 1];
+#pragma unroll
+    for (int k = 0; k < KM; ++k)
+      v[k] = (okj[0] ? u[0] * eh[k].x : 0.f) + (okj[1] ? u[1] * eh[k].y : 0.f) +
+             (okj[2] ? u[2] * eh[k].z : 0.f) + (okj[3] ? u[3] * eh[k].w : 0.f);
+    v[KM] = u[0] * wgu[0] + u[1] * wgu[1] + u[2] * wgu[2] + u[3] * wgu[3];
+#pragma unroll
+    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0xB1>(v[k]);
+#pragma unroll
+    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x4E>(v[k]);
+#pragma unroll
+    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x141>(v[k]);
+#pragma unroll
+    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x140>(v[k]);
+    // the four row sums: two lane-swap steps (no LDS memory access)
+#pragma unroll
+    for (int k = 0; k <= KM; ++k) v[k] += __shfl_xor(v[k], 16);
+#pragma unroll
+    for (int k = 0; k <= KM; ++k) v[k] += __shfl_xor(v[k], 32);
+    float s = v[KM] + a.b_g;
+#pragma unroll
+    for (int f = 0; f < 5; ++f) s += wgphi[f] * phi[f];
+    const float g = sig_alpha * sigmoidf_(s);
+    // residual of candidate (lane mod K): lanes < K score it, lanes K..2K-1 report it
+    const int kd = lane < K ? lane : lane - K;
+    float dk = 0.f;
+#pragma unroll
+    for (int k = 0; k < KM; ++k) dk = kd == k ? v[k] : dk;
+    const float lt = cl + g * (lane < K ? dk : 0.f);
+    const float m = wave_allmax(lane < K ? lt : -INFINITY);
+    const uint64_t hit = __ballot(lane < K && lt == m);
+    const int kstar = hit ? __builtin_ctzll(hit) : 0;
+    const int sel = __builtin_amdgcn_readlane(ci, kstar);
+    prev_x = readlane_f32(xs, kstar);
+    f4_t tz = lds_rd128(sv + (2u + KM + kstar) * 1024u), th = lds_rd128(sv + (2u + 2 * KM + kstar) * 1024u);
+    lds_drain();
+    after_drain(tz);
+    after_drain(th);
+    ptz[0] = okj[0] ? tz.x : 0.f; ptz[1] = okj[1] ? tz.y : 0.f;
+    ptz[2] = okj[2] ? tz.z : 0.f; ptz[3] = okj[3] ? tz.w : 0.f;
+    pth[0] = okj[0] ? th.x : 0.f; pth[1] = okj[1] ? th.y : 0.f;
+    pth[2] = okj[2] ? th.z : 0.f; pth[3] = okj[3] ? th.w : 0.f;
+    prev_tok = sel;
+    // one store instruction for every output of the row
+    const float ov = lane < K ? lt : (lane < 2 * K ? dk : (lane == 63 ? __int_as_float(sel) : g));
+    *out_ptr(row0 + i) = ov;
+  }
+  wait_vm_lgkm0<0>();  // no copy may land after the workgroup's LDS is released
+}
+
+// Vector stride of the step blocks: one 256-float vector per field when the
+// state fits (the single-wave scan copies whole 1 KiB vectors), else d_state.
+size_t step_vec_stride(int ds) { return ds <= 256 ? 256 : static_cast<size_t>(ds); }
+
 struct Layout {
-  size_t PE, PC, PH, U0, X, SB, TZA, THA, FZ, FH, total;
+  size_t PE, PC, PH, U0, X, SB, TZA, THA, FZ, FH, DUMP, total;
   size_t sPE, sPC, sPH, sU0;  // floats between split-K slices (multiples of 64)
   int splits;
 };
@@ -628,11 +882,12 @@ Layout rerank_layout(const brisk_corrector& c, int B, int L, int K) {
   l.PH = take(S * l.sPH);
   l.U0 = take(S * l.sU0);
   l.X = take(NP);
-  l.SB = take(rows * (2 + 3 * static_cast<size_t>(K)) * ds);
+  l.SB = take(rows * (2 + 3 * static_cast<size_t>(K)) * step_vec_stride(ds));
   l.TZA = take(static_cast<size_t>(B) * ds);
   l.THA = take(static_cast<size_t>(B) * ds);
   l.FZ = take(5 * ds);
   l.FH = take(5 * ds);
+  l.DUMP = take(static_cast<size_t>(B) * 64);
   l.total = off;
   return l;
 }
@@ -700,7 +955,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
 
   // Step blocks: row r holds F = 2 + 3K vectors [AZ, AH, EH_k, TZ_k, TH_k].
   const int FB = 2 + 3 * K;
-  const size_t blk = static_cast<size_t>(FB) * ds;
+  const size_t vsz = step_vec_stride(ds);
+  const size_t blk = static_cast<size_t>(FB) * vsz;
   float* SB = F(lay.SB);
   LiftJobs lj{};
   lj.ds = ds;
@@ -712,28 +968,33 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   const LiftTerm posz{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1};
   const LiftTerm posh{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1};
   const size_t vds = static_cast<size_t>(ds);
-  lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, NC, SB + (2 + K) * vds, K, blk};
-  lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, NC, SB + (2 + 2 * K) * vds, K, blk};
-  lj.job[2] = LiftJob{{fterm(F(lay.PC), c.rank, c.W_s, 1, ds), none}, NC, SB + 2 * vds, K, blk};
-  lj.job[3] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_z, d_in, 1), posz}, rows, SB, 1, blk};
-  lj.job[4] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_h, d_in, 1), posh}, rows, SB + vds, 1, blk};
-  lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, B, F(lay.TZA), 1, vds};
-  lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, B, F(lay.THA), 1, vds};
+  lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, NC, SB + (2 + K) * vsz, K, blk, vsz};
+  lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, NC, SB + (2 + 2 * K) * vsz, K, blk, vsz};
+  lj.job[2] = LiftJob{{fterm(F(lay.PC), c.rank, c.W_s, 1, ds), none}, NC, SB + 2 * vsz, K, blk, vsz};
+  lj.job[3] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_z, d_in, 1), posz}, rows, SB, 1, blk, vsz};
+  lj.job[4] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_h, d_in, 1), posh}, rows, SB + vsz, 1, blk, vsz};
+  lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, B, F(lay.TZA), 1, vds, vds};
+  lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, B, F(lay.THA), 1, vds, vds};
   // feature maps W_z[:, feat] P_phi and W_h[:, feat] P_phi as [5, ds]: input row f is column f of P_phi
-  lj.job[7] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1}, none}, 5, F(lay.FZ), 1, vds};
-  lj.job[8] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1}, none}, 5, F(lay.FH), 1, vds};
+  lj.job[7] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1}, none}, 5, F(lay.FZ), 1, vds, vds};
+  lj.job[8] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1}, none}, 5, F(lay.FH), 1, vds, vds};
   hipLaunchKernelGGL(lift_kernel, dim3((NC + LT_BN - 1) / LT_BN, (ds + LT_BJ - 1) / LT_BJ, kMaxLiftJobs),
                      dim3(256), 0, s, lj);
 
   ScanArgs sa{};
-  sa.B = B; sa.L = L; sa.K = K; sa.ds = ds;
+  sa.B = B; sa.L = L; sa.K = K; sa.ds = ds; sa.vs = static_cast<int>(vsz);
   sa.U0 = F(lay.U0); sa.X = F(lay.X); sa.SB = SB; sa.TZA = F(lay.TZA); sa.THA = F(lay.THA);
   sa.FZ = F(lay.FZ); sa.FH = F(lay.FH); sa.w_g = c.w_g;
   sa.alpha = c.alpha; sa.b_g = c.b_g;
   sa.cand_logit = cand_logit; sa.cand_id = cand_id; sa.anchor = anchor_tok;
   sa.selected = selected; sa.refined = refined; sa.gamma = gamma; sa.resid = resid;
+  sa.dump = F(lay.DUMP);
   const int nw = (ds + 63) / 64;
-  if (K <= 8) launch_scan<8, 4>(sa, B, nw, s);
+  if (ds <= 256 && K <= 8)
+    hipLaunchKernelGGL((scan_lds_kernel<8, 4>), dim3(B), dim3(64), 0, s, sa);
+  else if (ds <= 256 && K <= 16)
+    hipLaunchKernelGGL((scan_lds_kernel<16, 3>), dim3(B), dim3(64), 0, s, sa);
+  else if (K <= 8) launch_scan<8, 4>(sa, B, nw, s);
   else if (K <= 16) launch_scan<16, 3>(sa, B, nw, s);
   else launch_scan<64, 1>(sa, B, nw, s);
 }

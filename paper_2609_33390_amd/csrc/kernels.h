@@ -5,7 +5,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
-#include "../../include/brisk.h"
+#include "brisk.h"
 
 namespace brisk {
 

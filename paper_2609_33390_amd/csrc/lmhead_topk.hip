@@ -41,7 +41,10 @@ struct TileCfg {
   static constexpr int TPP = NT / BR;           // epilogue threads per position
   static constexpr int EPI_STRIDE = EPI_V + 4;  // floats per staged logit row
   static constexpr int EPI_BYTES = BR * EPI_STRIDE * 4;
-  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES + EPI_BYTES;
+  // The epilogue reuses the stage buffer of the slice just consumed when it
+  // fits (no copy targets that buffer until the next slice begins).
+  static constexpr bool EPI_ALIAS = EPI_BYTES <= STAGE_BYTES;
+  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES + (EPI_ALIAS ? 0 : EPI_BYTES);
   static_assert(ROWS % (RPI * NW) == 0 && BV % RPI == 0, "DMA instructions must tile the stage");
   static_assert(WV % 16 == 0 && WR % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(NT % BR == 0 && (TPP & (TPP - 1)) == 0, "epilogue thread mapping");
@@ -84,12 +87,13 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
 template <class C, int KP>
 constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 <= C::LDS_BYTES;
 
+// One workgroup per compute unit (the LDS footprint allows no more), so the
+// compiler may spend the whole register file on one wave per SIMD.
 template <class C, int KP>
-__global__ __launch_bounds__(C::NT) void lmhead_topk_kernel(
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void lmhead_topk_kernel(
     const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int rows, int d, int V,
     int n_rtiles, int n_vtiles, int tiles_per_group, uint64_t* __restrict__ partial, int n_parts) {
   __shared__ __align__(16) unsigned char smem[C::LDS_BYTES];
-  float* sE = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
 
   const int tid = threadIdx.x, lane = tid & 63;
   // the wave index is uniform per wave; saying so keeps LDS bases in scalars
@@ -185,17 +189,23 @@ __global__ __launch_bounds__(C::NT) void lmhead_topk_kernel(
       }
 #pragma unroll
       for (int kk = 0; kk < C::BK / 32; ++kk) {
-        bf16x8 b[C::TR];
+        // all operand fragments of this 32-wide slice first, then the MFMAs,
+        // so LDS latency overlaps the first products instead of every row
+        bf16x8 b[C::TR], a[C::TV];
 #pragma unroll
         for (int y = 0; y < C::TR; ++y)
           b[y] = *reinterpret_cast<const bf16x8*>(sb + (C::BV + wr * C::WR + y * 16) * C::CPR * 16 + lane_off[kk]);
 #pragma unroll
-        for (int x = 0; x < C::TV; ++x) {
-          const bf16x8 a = *reinterpret_cast<const bf16x8*>(sb + (wv * C::WV + x * 16) * C::CPR * 16 + lane_off[kk]);
+        for (int x = 0; x < C::TV; ++x)
+          a[x] = *reinterpret_cast<const bf16x8*>(sb + (wv * C::WV + x * 16) * C::CPR * 16 + lane_off[kk]);
+#pragma unroll
+        for (int x = 0; x < C::TV; ++x)
 #pragma unroll
           for (int y = 0; y < C::TR; ++y)
-            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b[y], acc[x][y], 0, 0, 0);
-        }
+            acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
+        // keep that order: every fragment read issued before the products
+        __builtin_amdgcn_sched_group_barrier(0x100, C::TV + C::TR, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, C::TV * C::TR, 0);
       }
     }
 
@@ -203,6 +213,13 @@ __global__ __launch_bounds__(C::NT) void lmhead_topk_kernel(
     // every wave as fp32 [position][wave_v * 16 + column]; each thread then
     // folds its position's columns into its running list.
     const int v0 = (vt_begin + tl) * C::BV;
+    float* sE;
+    if constexpr (C::EPI_ALIAS) {
+      sE = reinterpret_cast<float*>(smem + ((tl * nk + nk - 1) % C::STAGES) * C::STAGE_BYTES);
+      lds_sync();  // every wave has finished reading that slice
+    } else {
+      sE = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
+    }
 #pragma unroll
     for (int x = 0; x < C::TV; ++x) {
 #pragma unroll
