@@ -23,6 +23,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2516.6      # dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
 METRIC = "block positions/sec (propose+rerank+verify) and % HBM/MFMA roofline"
 DEFAULT_WORKLOAD = "llada8b-b1-l32"
+ROOT = os.path.dirname(os.path.abspath(__file__))
 
 
 def parse():
@@ -34,6 +35,8 @@ def parse():
     ap.add_argument("--graph", action="store_true", help="time hipGraph replay of the step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget-s", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run a 1 GiB streaming copy (for scaling HBM byte counters)")
     return ap.parse_args()
 
 
@@ -46,8 +49,9 @@ def propose_cost(wl):
 
 
 def cpu_baseline(blk, budget_s):
-    """The oracle, as is, on host cores: whole steps of the same workload,
-    repeated until the time budget is spent (at least one)."""
+    """The oracle, as is, on host cores, over a bounded sample of the same
+    workload: whole sequences of the batch (all L positions, propose + rerank +
+    verify), taken in order and repeated until the time budget is spent."""
     import numpy as np
     from threadpoolctl import threadpool_info
 
@@ -61,22 +65,71 @@ def cpu_baseline(blk, budget_s):
     x0 = blk.x0.cpu().numpy().astype(np.int64)
     ver = blk.verifier.cpu().numpy()
     psi = {k: oracle.bf16_to_f64(bf16_bits(blk.psi[k])) for k in PSI_FIELDS}
-    times = []
-    t_end = time.perf_counter() + budget_s
+    n_seq, positions, spent = 0, 0, 0.0
     while True:
+        b = n_seq % wl.B
+        rs = slice(b * wl.L, (b + 1) * wl.L)
         t0 = time.perf_counter()
-        cl, ci = oracle.propose_block(H_bits, W_bits, wl.K)
-        out = oracle.rerank(psi, blk.alpha, blk.b_g, H, h_c, x0, W_bits, E_bits, cl, ci, wl.B, wl.L)
-        oracle.verify_accept(out["selected"], ver)
-        times.append(time.perf_counter() - t0)
-        if time.perf_counter() >= t_end or len(times) >= 5:
+        cl, ci = oracle.propose_block(H_bits[rs], W_bits, wl.K)
+        out = oracle.rerank(psi, blk.alpha, blk.b_g, H[rs], h_c[b:b + 1], x0[b:b + 1], W_bits, E_bits,
+                            cl, ci, 1, wl.L)
+        oracle.verify_accept(out["selected"], ver[b:b + 1])
+        spent += time.perf_counter() - t0
+        n_seq += 1
+        positions += wl.L
+        if spent >= budget_s:
             break
     blas = [p.get("num_threads", 0) for p in threadpool_info() if p.get("user_api") == "blas"]
     cores = max(blas) if blas else 1
-    t = statistics.median(times)
-    return {"value": wl.B * wl.L / t, "unit": "block positions/s", "cores": cores, "kind": "oracle",
-            "sample": f"{len(times)} whole step(s) of {wl.name} ({wl.B * wl.L} positions), median "
-                      f"{t:.2f} s; float64 numpy, host has {os.cpu_count()} logical CPUs"}
+    return {"value": round(positions / spent, 2), "unit": "block positions/s", "cores": cores,
+            "kind": "oracle",
+            "sample": f"{n_seq} sequence(s) of {wl.name} ({positions} positions: propose + rerank + "
+                      f"verify, {spent:.1f} s); float64 numpy, host has {os.cpu_count()} logical CPUs"}
+
+
+def copy_calibration(n_bytes=1 << 30, reps=3):
+    """A plain streaming kernel of known size (read n_bytes, write n_bytes),
+    run so that HBM byte counters can be scaled against it."""
+    import torch
+
+    src = torch.ones(n_bytes // 4, dtype=torch.float32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration": {"kernel": "torch.neg (float32)", "read_bytes": n_bytes,
+                                           "write_bytes": n_bytes, "launches": reps}}), flush=True)
+
+
+def counter_traffic(wl):
+    """HBM bytes per brisk_propose_block call from the committed counter
+    summary of this workload, or None when it is missing or was taken on a
+    different version of the LM-head kernel source."""
+    path = os.path.join(ROOT, "profiles", f"traffic_propose_{wl.name}.txt")
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return round(float(vals["hbm_bytes_per_call"]))
+    except (KeyError, ValueError):
+        return None
+
+
+def kernel_source_hash():
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in ("lmhead_topk.hip", "device_common.h"):
+        with open(os.path.join(ROOT, "paper_2609_33390_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def main():
@@ -85,6 +138,9 @@ def main():
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the hot path is data parallel: see the sharding notes in DESIGN.md)", file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     import torch
 
     import paper_2609_33390_amd as brisk
@@ -178,7 +234,7 @@ def main():
         achieved = flops / t_prop / 1e12
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4)}
-    roof["traffic"] = None
+    roof["traffic"] = counter_traffic(wl)
     roof["kernel"] = "brisk_propose_block (lmhead_topk + topk_merge)"
     roof["launch_us"] = round(t_prop * 1e6, 2)
 
