@@ -227,7 +227,17 @@ __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
   const LiftJob& jb = jobs.job[blockIdx.z];
   const int n0 = blockIdx.x * LT_BN, j0 = blockIdx.y * LT_BJ;
   const int ds = jobs.ds;
-  if (n0 >= jb.n || j0 >= ds) return;
+  // vectors stored with a stride beyond d_state are zero-filled up to it
+  const int jend = static_cast<int>(jb.vs) > ds ? static_cast<int>(jb.vs) : ds;
+  if (n0 >= jb.n || j0 >= jend) return;
+  if (j0 >= ds) {
+    for (int e = threadIdx.x; e < LT_BN * LT_BJ; e += 256) {
+      const int n = n0 + e / LT_BJ, j = j0 + e % LT_BJ;
+      if (n < jb.n && j < jend)
+        jb.out[static_cast<size_t>(n / jb.grp) * jb.blk + static_cast<size_t>(n % jb.grp) * jb.vs + j] = 0.f;
+    }
+    return;
+  }
   __shared__ __align__(16) float s_in[LT_BC][LT_BN + 4];
   __shared__ __align__(16) float s_m[LT_BC][LT_BJ + 4];
   const int tid = threadIdx.x;
@@ -313,6 +323,7 @@ __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
     for (int y = 0; y < 4; ++y) {
       const int j = j0 + tj * 4 + y;
       if (j < ds) o[j] = acc[x][y];
+      else if (j < jend) o[j] = 0.f;
     }
   }
 }
@@ -590,14 +601,17 @@ __global__ __launch_bounds__(512) void scan_kernel(ScanArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// scan_lds: the whole sequence in one wavefront (d_state <= 256; lane l holds
-// state elements 4l..4l+3).  The step data of the next rows are copied into
-// an LDS ring straight from global memory - one buffer DMA instruction per
-// 1 KiB vector, and 64-word vectors for the candidate scores, ids and cross
-// logits - and the wave waits only for the row it is about to use.  After
-// the argmax, only the selected candidate's previous-token vectors are read
-// back.  Reductions: DPP inside each 16-lane row, then the four row sums meet
-// in LDS (a single wave needs no barrier for that).
+// scan_pc: one sequence per workgroup of two wavefronts (d_state <= 256).
+// Wave 1 is a copy engine: it streams the step blocks of the next rows into a
+// ring of D LDS slots with buffer-to-LDS DMA (one instruction per 1 KiB
+// vector, and 64-word vectors for the candidate logits, ids and cross
+// logits), waiting only for the row the recurrence is about to use.  Wave 0
+// runs the recurrence; lane l holds state elements 4l..4l+3.  One workgroup
+// barrier per row hands a filled slot to wave 0 and a consumed slot back to
+// wave 1, so the copies of later rows overlap the arithmetic of the current
+// one and neither wave spends issue slots on the other's work.
+// Step-block vectors are zero beyond d_state, so the padded state elements
+// stay zero without any masking in the loop.
 // ---------------------------------------------------------------------------
 template <int KM>
 struct LdsStage {
@@ -606,194 +620,169 @@ struct LdsStage {
   static constexpr int FLOATS = NVEC * 256 + 3 * 64;
 };
 
+// s_waitcnt vmcnt(N), leaving the other counters unconstrained.
 template <int N>
-__device__ __forceinline__ void wait_vm_lgkm0() {
-  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4) | (0 << 8));
+__device__ __forceinline__ void wait_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | (((N >> 4) & 3) << 14) | (7 << 4) | (15 << 8));
 }
+
+// Workgroup barrier that is also a compiler barrier for memory accesses (the
+// LDS reads after it must not be moved above it).
+__device__ __forceinline__ void wg_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 typedef __attribute__((address_space(3))) void* lds_vptr_t;
-
-// LDS reads of the copy ring, issued as inline assembly.  For an ordinary
-// LDS read the compiler cannot tell the ring slot apart from the slots still
-// being filled by copies and waits for every outstanding copy first, which
-// would undo the prefetch.  The reads here are followed by one explicit
-// lgkmcnt(0) wait; each value then passes through an empty asm ordered after
-// that wait, so no use can be scheduled before the data has arrived.
 typedef float f4_t __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ unsigned lds_addr(const float* p) {
-  return static_cast<unsigned>(reinterpret_cast<size_t>((const __attribute__((address_space(3))) float*)(p)));
+
+// DPP row broadcast into the rows selected by ROWMASK (others receive 0).
+template <int CTRL, int ROWMASK>
+__device__ __forceinline__ float dpp_rows(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, ROWMASK, 0xF, false));
 }
-__device__ __forceinline__ f4_t lds_rd128(unsigned addr) {
-  f4_t r;
-  asm volatile("ds_read_b128 %0, %1" : "=v"(r) : "v"(addr));
-  return r;
+
+__device__ __forceinline__ float sigmoid_rcp(float x) {
+  return __builtin_amdgcn_rcpf(1.0f + __expf(-x));
 }
-__device__ __forceinline__ float lds_rd32(unsigned addr) {
-  float r;
-  asm volatile("ds_read_b32 %0, %1" : "=v"(r) : "v"(addr));
-  return r;
-}
-__device__ __forceinline__ void lds_drain() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-template <class T>
-__device__ __forceinline__ void after_drain(T& x) { asm volatile("" : "+v"(x)); }
 
 template <int KM, int D>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void scan_lds_kernel(ScanArgs a) {
+__global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
   using S = LdsStage<KM>;
-  // Each row issues NDMA copies and one output store; waiting for row i
-  // leaves the copies of rows i+1..i+D-2 and the stores of rows i-D+1..i-1
-  // (issued after row i's copies) outstanding.
-  constexpr int kAfter = (D - 2) * S::NDMA + (D - 1);
-  static_assert(kAfter <= 63, "vmcnt range");
+  static_assert((D - 2) * S::NDMA <= 63, "vmcnt range");
   static_assert(2 * KM <= 62, "output lanes");
   __shared__ __align__(16) float ring[D * S::FLOATS];
-  const int lane = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
   const int b = blockIdx.x;
   const int ds = a.ds, K = a.K, L = a.L;
-  const int NC = a.B * L * K;
   const int F = 2 + 3 * K;
+  const size_t row0 = static_cast<size_t>(b) * L;
 
-  bool okj[4];
-  int ej[4];
+  if (wave == 1) {
+    // ---- copy engine --------------------------------------------------------
+    const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.SB + row0 * F * 256), static_cast<short>(0), L * F * 1024, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rcl = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.cand_logit + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rci = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<int32_t*>(a.cand_id + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rxs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(a.X + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+    // Copies of row i (clamped to the block) into slot i % D.  Candidate slots
+    // k >= K repeat candidate K-1, so every row issues exactly NDMA copies and
+    // vmcnt((D-2)*NDMA) always means "every row up to the one D-2 back landed".
+    auto issue = [&](int i) {
+      const int ii = i < L ? i : L - 1;
+      float* st = ring + (i % D) * S::FLOATS;
+      const unsigned rb = static_cast<unsigned>(ii * F) * 1024u;
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    okj[j] = 4 * lane + j < ds;
-    ej[j] = okj[j] ? 4 * lane + j : ds - 1;
+      for (int v = 0; v < S::NVEC; ++v) {
+        int f;
+        if (v < 2) f = v;
+        else if (v < 2 + KM) f = 2 + min(v - 2, K - 1);
+        else if (v < 2 + 2 * KM) f = 2 + K + min(v - 2 - KM, K - 1);
+        else f = 2 + 2 * K + min(v - 2 - 2 * KM, K - 1);
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_vptr_t)(st + v * 256), 16, lane * 16,
+                                                 rb + static_cast<unsigned>(f) * 1024u, 0, 0);
+      }
+      const unsigned cb = static_cast<unsigned>(ii * K) * 4u;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rcl, (lds_vptr_t)(st + S::NVEC * 256), 4, lane * 4, cb, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rci, (lds_vptr_t)(st + S::NVEC * 256 + 64), 4, lane * 4, cb, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_vptr_t)(st + S::NVEC * 256 + 128), 4, lane * 4, cb, 0, 0);
+    };
+#pragma unroll
+    for (int t = 0; t < D - 1; ++t) issue(t);
+    for (int i = 0; i < L; ++i) {
+      wait_vm<(D - 2) * S::NDMA>();  // row i has landed
+      wg_barrier();                  // hand slot i over; slot (i-1) % D is free again
+      issue(i + D - 1);
+    }
+    wait_vm<0>();  // no copy may land after the workgroup's LDS is released
+    return;
   }
-  float u[4], wgu[4], fz[4][5], fh[4][5], ptz[4], pth[4];
+
+  // ---- recurrence (wave 0) ---------------------------------------------------
+  float u[4], wgu[4], fz[4][5], fh[4][5];
+  f4_t ptz, pth;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    const float u0a = a.U0[static_cast<size_t>(b) * ds + ej[j]];
-    const float u0b = a.U0[static_cast<size_t>(a.B + b) * ds + ej[j]];
-    u[j] = okj[j] ? tanhf(u0a + u0b) : 0.f;
-    wgu[j] = okj[j] ? bf16_to_f32(a.w_g[ej[j]]) : 0.f;
-    const float tz = a.TZA[static_cast<size_t>(b) * ds + ej[j]], th = a.THA[static_cast<size_t>(b) * ds + ej[j]];
-    ptz[j] = okj[j] ? tz : 0.f;
-    pth[j] = okj[j] ? th : 0.f;
+    const bool ok = 4 * lane + j < ds;
+    const int e = ok ? 4 * lane + j : ds - 1;
+    const float u0a = a.U0[static_cast<size_t>(b) * ds + e];
+    const float u0b = a.U0[static_cast<size_t>(a.B + b) * ds + e];
+    u[j] = ok ? tanhf(u0a + u0b) : 0.f;
+    wgu[j] = ok ? bf16_to_f32(a.w_g[e]) : 0.f;
+    const float tz = a.TZA[static_cast<size_t>(b) * ds + e], th = a.THA[static_cast<size_t>(b) * ds + e];
+    ptz[j] = ok ? tz : 0.f;
+    pth[j] = ok ? th : 0.f;
 #pragma unroll
     for (int f = 0; f < 5; ++f) {
-      const float z = a.FZ[f * ds + ej[j]], h = a.FH[f * ds + ej[j]];
-      fz[j][f] = okj[j] ? z : 0.f;
-      fh[j][f] = okj[j] ? h : 0.f;
+      const float z = a.FZ[f * ds + e], h = a.FH[f * ds + e];
+      fz[j][f] = ok ? z : 0.f;
+      fh[j][f] = ok ? h : 0.f;
     }
   }
   float wgphi[5];
 #pragma unroll
   for (int f = 0; f < 5; ++f) wgphi[f] = bf16_to_f32(a.w_g[ds + f]);
   const float sig_alpha = sigmoidf_(a.alpha);
-  float prev_x = a.X[NC + b];
+  const float b_g = a.b_g;
+  float prev_x = a.X[static_cast<size_t>(a.B) * L * K + b];
   int prev_tok = a.anchor[b];
-  // materialise the set-up values here (the compiler would otherwise sink
-  // their loads into the loop), then start counting copies from an empty queue
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    asm volatile("" : "+v"(u[j]), "+v"(wgu[j]), "+v"(ptz[j]), "+v"(pth[j]));
-#pragma unroll
-    for (int f = 0; f < 5; ++f) asm volatile("" : "+v"(fz[j][f]), "+v"(fh[j][f]));
-  }
-  asm volatile("" : "+v"(prev_x), "+v"(prev_tok));
-  wait_vm_lgkm0<0>();
 
-  const size_t row0 = static_cast<size_t>(b) * L;
-  const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(a.SB + row0 * F * 256), static_cast<short>(0), L * F * 1024, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rcl = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(a.cand_logit + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rci = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<int32_t*>(a.cand_id + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
-  const __amdgpu_buffer_rsrc_t rxs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(a.X + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+  // Each lane stores one value per row: lanes < K the refined logits, lanes
+  // K..2K-1 the residuals, lane 62 the gate, lane 63 the selected id; lanes
+  // without an output (or whose output was not requested) write to a sink.
+  const bool want = a.refined != nullptr || a.resid != nullptr;
+  const int kd = lane < K ? lane : lane - K;
+  float* obase = a.dump + static_cast<size_t>(b) * 64 + lane;
+  size_t ostride = 0;
+  if (lane < K && a.refined) { obase = a.refined + lane; ostride = K; }
+  else if (lane >= K && lane < 2 * K && a.resid) { obase = a.resid + (lane - K); ostride = K; }
+  else if (lane == 62 && a.gamma) { obase = a.gamma; ostride = 1; }
+  else if (lane == 63) { obase = reinterpret_cast<float*>(a.selected); ostride = 1; }
 
-  // Copies of row i (clamped to the block) into ring slot i % D.  Candidate
-  // slots k >= K repeat candidate K-1 so every row issues exactly NDMA copies.
-  auto issue = [&](int i) {
-    const int ii = i < L ? i : L - 1;
-    float* st = ring + (i % D) * S::FLOATS;
-    const unsigned rb = static_cast<unsigned>(ii * F) * 1024u;
-#pragma unroll
-    for (int v = 0; v < S::NVEC; ++v) {
-      int f;
-      if (v < 2) f = v;
-      else if (v < 2 + KM) f = 2 + min(v - 2, K - 1);
-      else if (v < 2 + 2 * KM) f = 2 + K + min(v - 2 - KM, K - 1);
-      else f = 2 + 2 * K + min(v - 2 - 2 * KM, K - 1);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_vptr_t)(st + v * 256), 16, lane * 16,
-                                               rb + static_cast<unsigned>(f) * 1024u, 0, 0);
-    }
-    const unsigned cb = static_cast<unsigned>(ii * K) * 4u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rcl, (lds_vptr_t)(st + S::NVEC * 256), 4, lane * 4, cb, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rci, (lds_vptr_t)(st + S::NVEC * 256 + 64), 4, lane * 4, cb, 0, 0);
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_vptr_t)(st + S::NVEC * 256 + 128), 4, lane * 4, cb, 0, 0);
-  };
-
-  // where this lane writes its output of a row (see the store below)
-  float* const dump = a.dump + static_cast<size_t>(b) * 64 + lane;
-  auto out_ptr = [&](size_t r) -> float* {
-    if (lane < K) return a.refined ? a.refined + r * K + lane : dump;
-    if (lane < 2 * K) return a.resid ? a.resid + r * K + (lane - K) : dump;
-    if (lane == 62) return a.gamma ? a.gamma + r : dump;
-    if (lane == 63) return reinterpret_cast<float*>(a.selected + r);
-    return dump;
-  };
-
-  // Prologue: the first D-1 rows, each followed by a store to the sink so the
-  // queue already has the steady-state shape (copies of a row, then one store).
-#pragma unroll
-  for (int t = 0; t < D - 1; ++t) {
-    issue(t);
-    *dump = 0.f;
-  }
   for (int i = 0; i < L; ++i) {
-    wait_vm_lgkm0<kAfter>();  // row i has landed; reads of slot (i-1) % D are done
-    issue(i + D - 1);
+    wg_barrier();  // row i is in slot i % D
     const float* st = ring + (i % D) * S::FLOATS;
-    const unsigned sv = lds_addr(st) + 16u * lane, sw = lds_addr(st) + 4u * lane;
-    f4_t az = lds_rd128(sv), ah = lds_rd128(sv + 1024u);
+    const f4_t* sv = reinterpret_cast<const f4_t*>(st) + lane;  // vector v of the row at sv[64 v]
+    const float* sc = st + S::NVEC * 256;                          // logits, ids, cross logits
+    const f4_t az = sv[0], ah = sv[64];
     f4_t eh[KM];
 #pragma unroll
-    for (int k = 0; k < KM; ++k) eh[k] = lds_rd128(sv + (2u + k) * 1024u);
-    float cl = lds_rd32(sw + S::NVEC * 1024u);
-    float cif = lds_rd32(sw + S::NVEC * 1024u + 256u);
-    float xs = lds_rd32(sw + S::NVEC * 1024u + 512u);
-    lds_drain();
-    after_drain(az);
-    after_drain(ah);
+    for (int k = 0; k < KM; ++k) eh[k] = sv[64 * (2 + k)];
+    const float cl_l = sc[lane], xs_l = sc[128 + lane];
+    const int ci_l = __float_as_int(sc[64 + lane]);
+    float clu[KM];  // every lane reads the same words: the candidate logits as uniform values
 #pragma unroll
-    for (int k = 0; k < KM; ++k) after_drain(eh[k]);
-    after_drain(cl);
-    after_drain(cif);
-    after_drain(xs);
-    const int ci = __float_as_int(cif);
+    for (int k = 0; k < KM; ++k) clu[k] = sc[k];
+    int idu[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) idu[k] = __float_as_int(sc[64 + k]);
 
-    const float c0 = readlane_f32(cl, 0), c1 = readlane_f32(cl, 1), c3 = readlane_f32(cl, 3);
-    const int id0 = __builtin_amdgcn_readlane(ci, 0);
-    const bool in4 = __ballot(lane < 4 && ci == prev_tok) != 0;
     float phi[5];
-    phi[0] = c0 - c1;
-    phi[1] = c0 - c3;
-    phi[2] = prev_tok == id0 ? 1.f : 0.f;
-    phi[3] = in4 ? 1.f : 0.f;
-    phi[4] = c0 - prev_x;
+    phi[0] = clu[0] - clu[1];
+    phi[1] = clu[0] - clu[3];
+    phi[2] = prev_tok == idu[0] ? 1.f : 0.f;
+    phi[3] = (prev_tok == idu[0] || prev_tok == idu[1] || prev_tok == idu[2] || prev_tok == idu[3]) ? 1.f : 0.f;
+    phi[4] = clu[0] - prev_x;
 
-    const float azv[4] = {az.x, az.y, az.z, az.w}, ahv[4] = {ah.x, ah.y, ah.z, ah.w};
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      float gz = azv[j] + ptz[j], gh = ahv[j] + pth[j];
+      float gz = az[j] + ptz[j], gh = ah[j] + pth[j];
 #pragma unroll
       for (int f = 0; f < 5; ++f) {
         gz += fz[j][f] * phi[f];
         gh += fh[j][f] * phi[f];
       }
-      const float z = sigmoidf_(gz);
-      u[j] = okj[j] ? (1.f - z) * u[j] + z * gh : 0.f;
+      const float z = sigmoid_rcp(gz);
+      u[j] = (1.f - z) * u[j] + z * gh;
     }
 
     float v[KM + 1];
 #pragma unroll
-    for (int k = 0; k < KM; ++k)
-      v[k] = (okj[0] ? u[0] * eh[k].x : 0.f) + (okj[1] ? u[1] * eh[k].y : 0.f) +
-             (okj[2] ? u[2] * eh[k].z : 0.f) + (okj[3] ? u[3] * eh[k].w : 0.f);
+    for (int k = 0; k < KM; ++k) v[k] = u[0] * eh[k][0] + u[1] * eh[k][1] + u[2] * eh[k][2] + u[3] * eh[k][3];
     v[KM] = u[0] * wgu[0] + u[1] * wgu[1] + u[2] * wgu[2] + u[3] * wgu[3];
+    // 64-lane sums: DPP inside each 16-lane row, then row broadcasts gather
+    // the four row sums into lane 63
 #pragma unroll
     for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0xB1>(v[k]);
 #pragma unroll
@@ -802,40 +791,45 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(1, 1))) void
     for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x141>(v[k]);
 #pragma unroll
     for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x140>(v[k]);
-    // the four row sums: two lane-swap steps (no LDS memory access)
 #pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += __shfl_xor(v[k], 16);
+    for (int k = 0; k <= KM; ++k) v[k] += dpp_rows<0x142, 0xA>(v[k]);  // row_bcast:15
 #pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += __shfl_xor(v[k], 32);
-    float s = v[KM] + a.b_g;
+    for (int k = 0; k <= KM; ++k) v[k] += dpp_rows<0x143, 0xC>(v[k]);  // row_bcast:31
+    float dk[KM];
+#pragma unroll
+    for (int k = 0; k < KM; ++k) dk[k] = readlane_f32(v[k], 63);
+    float s = readlane_f32(v[KM], 63) + b_g;
 #pragma unroll
     for (int f = 0; f < 5; ++f) s += wgphi[f] * phi[f];
-    const float g = sig_alpha * sigmoidf_(s);
-    // residual of candidate (lane mod K): lanes < K score it, lanes K..2K-1 report it
-    const int kd = lane < K ? lane : lane - K;
-    float dk = 0.f;
+    const float g = sig_alpha * sigmoid_rcp(s);
+
+    // refined logits and their argmax (the first maximum: smallest k on ties)
+    float best = __builtin_fmaf(g, dk[0], clu[0]);
+    int kb = 0;
 #pragma unroll
-    for (int k = 0; k < KM; ++k) dk = kd == k ? v[k] : dk;
-    const float lt = cl + g * (lane < K ? dk : 0.f);
-    const float m = wave_allmax(lane < K ? lt : -INFINITY);
-    const uint64_t hit = __ballot(lane < K && lt == m);
-    const int kstar = hit ? __builtin_ctzll(hit) : 0;
-    const int sel = __builtin_amdgcn_readlane(ci, kstar);
-    prev_x = readlane_f32(xs, kstar);
-    f4_t tz = lds_rd128(sv + (2u + KM + kstar) * 1024u), th = lds_rd128(sv + (2u + 2 * KM + kstar) * 1024u);
-    lds_drain();
-    after_drain(tz);
-    after_drain(th);
-    ptz[0] = okj[0] ? tz.x : 0.f; ptz[1] = okj[1] ? tz.y : 0.f;
-    ptz[2] = okj[2] ? tz.z : 0.f; ptz[3] = okj[3] ? tz.w : 0.f;
-    pth[0] = okj[0] ? th.x : 0.f; pth[1] = okj[1] ? th.y : 0.f;
-    pth[2] = okj[2] ? th.z : 0.f; pth[3] = okj[3] ? th.w : 0.f;
+    for (int k = 1; k < KM; ++k) {
+      const float lt = __builtin_fmaf(g, dk[k], clu[k]);
+      const bool take = k < K && lt > best;
+      best = take ? lt : best;
+      kb = take ? k : kb;
+    }
+    const int kstar = __builtin_amdgcn_readfirstlane(kb);
+    const int sel = __builtin_amdgcn_readlane(ci_l, kstar);
+    prev_x = readlane_f32(xs_l, kstar);
+    ptz = sv[64 * (2 + KM + kstar)];
+    pth = sv[64 * (2 + 2 * KM + kstar)];
     prev_tok = sel;
-    // one store instruction for every output of the row
-    const float ov = lane < K ? lt : (lane < 2 * K ? dk : (lane == 63 ? __int_as_float(sel) : g));
-    *out_ptr(row0 + i) = ov;
+
+    float ov = g;
+    if (want) {
+      float dl = dk[0];
+#pragma unroll
+      for (int k = 1; k < KM; ++k) dl = kd == k ? dk[k] : dl;
+      ov = lane < K ? __builtin_fmaf(g, dl, cl_l) : (lane < 2 * K ? dl : g);
+    }
+    ov = lane == 63 ? __int_as_float(sel) : ov;
+    obase[(row0 + i) * ostride] = ov;
   }
-  wait_vm_lgkm0<0>();  // no copy may land after the workgroup's LDS is released
 }
 
 // Vector stride of the step blocks: one 256-float vector per field when the
@@ -978,7 +972,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   // feature maps W_z[:, feat] P_phi and W_h[:, feat] P_phi as [5, ds]: input row f is column f of P_phi
   lj.job[7] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1}, none}, 5, F(lay.FZ), 1, vds, vds};
   lj.job[8] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1}, none}, 5, F(lay.FH), 1, vds, vds};
-  hipLaunchKernelGGL(lift_kernel, dim3((NC + LT_BN - 1) / LT_BN, (ds + LT_BJ - 1) / LT_BJ, kMaxLiftJobs),
+  const int lift_cols = static_cast<int>(vsz > vds ? vsz : vds);
+  hipLaunchKernelGGL(lift_kernel, dim3((NC + LT_BN - 1) / LT_BN, (lift_cols + LT_BJ - 1) / LT_BJ, kMaxLiftJobs),
                      dim3(256), 0, s, lj);
 
   ScanArgs sa{};
@@ -991,9 +986,9 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   sa.dump = F(lay.DUMP);
   const int nw = (ds + 63) / 64;
   if (ds <= 256 && K <= 8)
-    hipLaunchKernelGGL((scan_lds_kernel<8, 4>), dim3(B), dim3(64), 0, s, sa);
+    hipLaunchKernelGGL((scan_pc_kernel<8, 4>), dim3(B), dim3(128), 0, s, sa);
   else if (ds <= 256 && K <= 16)
-    hipLaunchKernelGGL((scan_lds_kernel<16, 3>), dim3(B), dim3(64), 0, s, sa);
+    hipLaunchKernelGGL((scan_pc_kernel<16, 3>), dim3(B), dim3(128), 0, s, sa);
   else if (K <= 8) launch_scan<8, 4>(sa, B, nw, s);
   else if (K <= 16) launch_scan<16, 3>(sa, B, nw, s);
   else launch_scan<64, 1>(sa, B, nw, s);
