@@ -42,6 +42,13 @@ __device__ __forceinline__ int32_t key_id(uint64_t key) {
   return static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(key));
 }
 
+// Smallest logit that can still enter a list whose last entry is `last`
+// (any finite logit while the list has an empty slot).  A logit equal to it
+// may enter or not depending on its id, so callers compare with >=.
+__device__ __forceinline__ float list_floor(uint64_t last) {
+  return last == 0 ? -INFINITY : key_logit(last);
+}
+
 // Insert `key` into a list sorted descending, dropping the smallest entry.
 // Branch-free: every slot keeps max(slot, carry) and passes min on.
 template <int N>

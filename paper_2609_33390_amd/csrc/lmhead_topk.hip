@@ -39,8 +39,7 @@ struct TileCfg {
   static constexpr int NDMA = ROWS / RPI / NW;  // DMA instructions per wave per stage
   static constexpr int STAGE_BYTES = ROWS * BK * 2;
   static constexpr int TPP = NT / BR;           // epilogue threads per position
-  static constexpr int EPI_STRIDE = EPI_V + 4;  // floats per staged logit row
-  static constexpr int EPI_BYTES = BR * EPI_STRIDE * 4;
+  static constexpr int EPI_BYTES = BR * EPI_V * 4;  // staged logits, [BR][EPI_V] fp32
   // The epilogue reuses the stage buffer of the slice just consumed when it
   // fits (no copy targets that buffer until the next slice begins).
   static constexpr bool EPI_ALIAS = EPI_BYTES <= STAGE_BYTES;
@@ -49,16 +48,26 @@ struct TileCfg {
   static_assert(WV % 16 == 0 && WR % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(NT % BR == 0 && (TPP & (TPP - 1)) == 0, "epilogue thread mapping");
   static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8), "reduction slice");
-  static_assert(EPI_V % (4 * TPP) == 0, "epilogue chunking");
+  static_assert(EPI_V % (4 * TPP) == 0 && EPI_V >= 32, "epilogue chunking");
   static_assert((STAGES - 2) * NDMA <= 63, "vmcnt range");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
 
-// 16-byte slot that holds chunk c of staged row r (an involution in c).
+// 16-byte slot that holds chunk c of staged row r (an involution in c).  A
+// 128-bit LDS read is served 8 lanes at a time; the MFMA operand reads put 8
+// consecutive rows at one chunk in such a group, so the eight rows of every
+// aligned run of 8 must land on eight different 16-byte bank groups (rows are
+// CPR * 16 bytes long, so a bank line of 128 bytes holds 8 / CPR rows).
 template <int CPR>
 __device__ __forceinline__ int swz(int r, int c) {
-  return c ^ ((r / (16 / CPR)) & (CPR - 1));
+  return c ^ ((r / (8 / CPR)) & (CPR - 1));
 }
+
+// 16-byte slot of chunk c (four logits) in staged logit row p: rows are
+// EPI_V * 4 bytes long, and the eight rows of an aligned run of 8 put a given
+// chunk on eight different bank groups (writes come 16 rows per chunk, reads
+// one row per thread).
+__device__ __forceinline__ int epi_slot(int p, int c) { return c ^ (p & 7); }
 
 // Wait until at most N vector-memory operations of this thread are
 // outstanding and all its LDS operations are done, then barrier.
@@ -88,9 +97,9 @@ template <class C, int KP>
 constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 <= C::LDS_BYTES;
 
 // One workgroup per compute unit (the LDS footprint allows no more), so the
-// compiler may spend the whole register file on one wave per SIMD.
+// compiler may split the whole register file among the workgroup's waves.
 template <class C, int KP>
-__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) void lmhead_topk_kernel(
+__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4, C::NW / 4))) void lmhead_topk_kernel(
     const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int rows, int d, int V,
     int n_rtiles, int n_vtiles, int tiles_per_group, uint64_t* __restrict__ partial, int n_parts) {
   __shared__ __align__(16) unsigned char smem[C::LDS_BYTES];
@@ -118,16 +127,11 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) v
   const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(H), static_cast<short>(0), static_cast<int>(static_cast<unsigned>(rows) * d * 2u), 0x00020000);
   const unsigned row_bytes = static_cast<unsigned>(d) * 2u;
-  // lane part of a copy's byte offset: row lane / CPR of the instruction's rows,
-  // the chunk its slot holds (the swizzle phase depends on the parity of the
-  // instruction's first row block when CPR = 8)
-  unsigned lane_voff[2];
-#pragma unroll
-  for (int par = 0; par < 2; ++par) {
-    const int R = par * C::RPI + lane / C::CPR;
-    lane_voff[par] = static_cast<unsigned>(lane / C::CPR) * row_bytes +
-                     static_cast<unsigned>(swz<C::CPR>(R, lane % C::CPR)) * 16u;
-  }
+  // lane part of a copy's byte offset: row lane / CPR of the instruction's
+  // rows, and the chunk its slot holds (the swizzle repeats every 8 rows, so
+  // it does not depend on the instruction)
+  const unsigned lane_voff = static_cast<unsigned>(lane / C::CPR) * row_bytes +
+                             static_cast<unsigned>(swz<C::CPR>(lane / C::CPR, lane % C::CPR)) * 16u;
   auto issue = [&](int g) {
     int tl = g / nk, kt = g % nk;
     if (tl >= n_tiles) {
@@ -139,7 +143,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) v
 #pragma unroll
     for (int i = 0; i < C::NDMA; ++i) {
       const int j = i * C::NW + wave;
-      const unsigned lv = lane_voff[C::CPR == 8 ? (j & 1) : 0];
+      const unsigned lv = lane_voff;
       if (j * C::RPI < C::BV) {
         const unsigned off = lv + (v0 + static_cast<unsigned>(j * C::RPI)) * row_bytes + k0b;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(base + j * 1024), 16, off, 0, 0, 0);
@@ -155,12 +159,13 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) v
   int lane_off[C::BK / 32];
 #pragma unroll
   for (int kk = 0; kk < C::BK / 32; ++kk)
-    lane_off[kk] = (l15 * C::CPR + ((kk * 4 + (lane >> 4)) ^ (l15 / (16 / C::CPR)))) * 16;
+    lane_off[kk] = (l15 * C::CPR + swz<C::CPR>(l15, kk * 4 + (lane >> 4))) * 16;
 
   const int ep = tid % C::BR, esub = tid / C::BR;
   uint64_t list[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
+  float thr = -INFINITY;  // logits below this cannot enter the list
 
   floatx4 acc[C::TV][C::TR];
 #pragma unroll
@@ -225,19 +230,25 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(1, 1))) v
 #pragma unroll
       for (int y = 0; y < C::TR; ++y) {
         const int p = wr * C::WR + y * 16 + l15;
-        *reinterpret_cast<floatx4*>(sE + p * C::EPI_STRIDE + wv * 16 + (lane >> 4) * 4) = acc[x][y];
+        *reinterpret_cast<floatx4*>(sE + p * C::EPI_V + epi_slot(p, wv * 4 + (lane >> 4)) * 4) = acc[x][y];
         acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
       lds_sync();
 #pragma unroll
       for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) {
-        const floatx4 v = *reinterpret_cast<const floatx4*>(sE + ep * C::EPI_STRIDE + col);
-        const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);
+        const floatx4 v = *reinterpret_cast<const floatx4*>(sE + ep * C::EPI_V + epi_slot(ep, col >> 2) * 4);
+        // common case: none of the four logits reaches the list's smallest
+        // entry, which one float compare decides; only then build keys
+        const float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+        if (m >= thr) {
+          const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int vid = vid0 + q;
-          const uint64_t key = make_key(v[q], static_cast<uint32_t>(vid));
-          if (vid < V && key > list[KP - 1]) list_insert(list, key);
+          for (int q = 0; q < 4; ++q) {
+            const int vid = vid0 + q;
+            const uint64_t key = make_key(v[q], static_cast<uint32_t>(vid));
+            if (vid < V && key > list[KP - 1]) list_insert(list, key);
+          }
+          thr = list_floor(list[KP - 1]);
         }
       }
       lds_sync();
@@ -333,7 +344,7 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
 
 using SmallRows = TileCfg<256, 32, 4, 1, 64, 3>;    // <= 32 rows: weight streaming
 using MidRows = TileCfg<256, 64, 4, 1, 64, 3>;      // <= 64 rows
-using LargeRows = TileCfg<256, 256, 2, 2, 32, 3>;   // many rows: MFMA bound
+using LargeRows = TileCfg<256, 256, 2, 4, 64, 2>;   // many rows: MFMA bound
 
 constexpr int kTargetWorkgroups = 256;  // one persistent workgroup per compute unit
 
