@@ -344,7 +344,7 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
 
 using SmallRows = TileCfg<256, 32, 4, 1, 64, 3>;    // <= 32 rows: weight streaming
 using MidRows = TileCfg<256, 64, 4, 1, 64, 3>;      // <= 64 rows
-using LargeRows = TileCfg<256, 256, 2, 4, 64, 2>;   // many rows: MFMA bound
+using LargeRows = TileCfg<256, 256, 4, 2, 64, 2>;   // many rows: MFMA bound
 
 constexpr int kTargetWorkgroups = 256;  // one persistent workgroup per compute unit
 
