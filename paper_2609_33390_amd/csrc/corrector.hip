@@ -189,12 +189,20 @@ __global__ __launch_bounds__(256) void cross_dot_kernel(const uint16_t* __restri
 
 // ---------------------------------------------------------------------------
 // lift: out[n, j] = sum over terms T of sum_c M_T(j, c) in_T(n, c), j < ds.
-// A term reads its input either as fp32 (the projections above) or as bf16
-// (the position table, the feature map P_phi), with arbitrary strides and an
-// optional row period (position index = row mod L); M_T(j, c) =
-// m[j * m_rs + c * m_cs] is a bf16 slice of a corrector matrix.  Tiles of
-// 32 rows x 64 outputs, 2 x 4 outputs per thread; the reduction is staged in
-// LDS 32 columns at a time with the next columns already loading.
+// A term reads its input either as fp32 (the projections above, split-K
+// slices already summed) or as bf16 (the position table, the feature map
+// P_phi), with arbitrary strides and an optional row period (position index
+// = row mod L); M_T(j, c) = m[j * m_rs + c * m_cs] is a bf16 slice of a
+// corrector matrix.
+//
+// MFMA with a three-term split of the fp32 input: x = x0 + x1 + x2 + e with
+// x0 = bf16(x), x1 = bf16(x - x0), x2 = bf16(x - x0 - x1) and |e| <= 2^-27
+// |x|, so M x = M x0 + M x1 + M x2 goes through bf16 products with fp32
+// accumulation at full fp32 input precision (the matrices are bf16
+// already).  Tiles of 64 rows x 64 outputs (wave w owns outputs
+// 16w..16w+15 of the tile); the reduction is staged in LDS 64 columns at a
+// time with the next columns already loading.  Vectors stored with a stride
+// beyond d_state are zero-filled up to the stride.
 // ---------------------------------------------------------------------------
 struct LiftTerm {
   const void* in;      // fp32 or bf16
@@ -203,6 +211,8 @@ struct LiftTerm {
   int C;
   const uint16_t* m;
   int m_rs, m_cs;
+  int vec;    // fp32 input rows may be read as 16-byte vectors along c
+  int mvec;   // the matrix may be read as 16-byte vectors along its contiguous index
 };
 struct LiftJob {
   LiftTerm t[2];       // second term optional (C = 0)
@@ -216,7 +226,13 @@ struct LiftJobs {
   LiftJob job[kMaxLiftJobs];
   int ds;
 };
-constexpr int LT_BN = 32, LT_BJ = 64, LT_BC = 32;
+constexpr int LT_BN = 64, LT_BJ = 64, LT_BC = 64, LT_ROW = LT_BC + 8;  // LDS row: 144 bytes
+
+__device__ __forceinline__ uint16_t bf16_rne(float x) {
+  uint32_t u = __float_as_uint(x);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
 
 __device__ __forceinline__ float lift_in(const LiftTerm& t, int n, int c) {
   const size_t idx = static_cast<size_t>(t.period ? n % t.period : n) * t.rs + static_cast<size_t>(c) * t.cs;
@@ -227,102 +243,148 @@ __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
   const LiftJob& jb = jobs.job[blockIdx.z];
   const int n0 = blockIdx.x * LT_BN, j0 = blockIdx.y * LT_BJ;
   const int ds = jobs.ds;
-  // vectors stored with a stride beyond d_state are zero-filled up to it
   const int jend = static_cast<int>(jb.vs) > ds ? static_cast<int>(jb.vs) : ds;
   if (n0 >= jb.n || j0 >= jend) return;
-  if (j0 >= ds) {
-    for (int e = threadIdx.x; e < LT_BN * LT_BJ; e += 256) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  auto out_row = [&](int n) {
+    return jb.out + static_cast<size_t>(n / jb.grp) * jb.blk + static_cast<size_t>(n % jb.grp) * jb.vs;
+  };
+  if (j0 >= ds) {  // zero padding only
+    for (int e = tid; e < LT_BN * LT_BJ; e += 256) {
       const int n = n0 + e / LT_BJ, j = j0 + e % LT_BJ;
-      if (n < jb.n && j < jend)
-        jb.out[static_cast<size_t>(n / jb.grp) * jb.blk + static_cast<size_t>(n % jb.grp) * jb.vs + j] = 0.f;
+      if (n < jb.n && j < jend) out_row(n)[j] = 0.f;
     }
     return;
   }
-  __shared__ __align__(16) float s_in[LT_BC][LT_BN + 4];
-  __shared__ __align__(16) float s_m[LT_BC][LT_BJ + 4];
-  const int tid = threadIdx.x;
-  const int tn = tid & 15, tj = tid >> 4;
+
+  __shared__ __align__(16) uint16_t s_x[3][2][LT_BN * LT_ROW];
+  __shared__ __align__(16) uint16_t s_m[2][LT_BJ * LT_ROW];
+
   const int CA = jb.t[0].C, c_total = CA + jb.t[1].C;
-  float acc[2][4];
+  const int nch = (c_total + LT_BC - 1) / LT_BC;
+  // staging map: 16 consecutive columns of one row per thread
+  const int sr = tid >> 2, sc = (tid & 3) * 16;
+  // a matrix stored along j (m_rs == 1) is read along j and transposed
+  const bool mt = jb.t[0].m_rs == 1;
+  float rin[16];
+  uint16_t rm[16];
+  // 16-element runs that stay inside one term and are 16-byte aligned load
+  // as vectors (the host sets vec / mvec when strides and offsets allow it)
+  auto load = [&](int ch) {
+    const int n = n0 + sr;
+    const int cb = ch * LT_BC + sc;  // first column of this thread's run
+    const LiftTerm& t0 = jb.t[0];
+    if (t0.vec && n < jb.n && cb + 16 <= CA) {
+      const float* p = static_cast<const float*>(t0.in) + static_cast<size_t>(n) * t0.rs + cb;
 #pragma unroll
-  for (int x = 0; x < 2; ++x)
-#pragma unroll
-    for (int y = 0; y < 4; ++y) acc[x][y] = 0.f;
-
-  float rin[4], rm[8];
-  auto load = [&](int c0) {
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = tid + q * 256;
-      const int cc = e & (LT_BC - 1), rr = e >> 5;
-      const int c = c0 + cc, n = n0 + rr;
-      float v = 0.f;
-      if (n < jb.n && c < c_total) v = c < CA ? lift_in(jb.t[0], n, c) : lift_in(jb.t[1], n, c - CA);
-      rin[q] = v;
-    }
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + q * 256;
-      // walk along whichever index is contiguous in memory (decided by the
-      // first term for the whole tile, so every thread agrees on the mapping)
-      const bool jfast = jb.t[0].m_rs == 1;
-      const int cc = jfast ? (e >> 6) : (e & (LT_BC - 1));
-      const int rr = jfast ? (e & 63) : (e >> 5);
-      const int cx = c0 + cc, j = j0 + rr;
-      float v = 0.f;
-      if (j < ds && cx < c_total) {
-        const LiftTerm& tt = cx < CA ? jb.t[0] : jb.t[1];
-        const int cl = cx < CA ? cx : cx - CA;
-        v = bf16_to_f32(tt.m[static_cast<size_t>(j) * tt.m_rs + static_cast<size_t>(cl) * tt.m_cs]);
+      for (int v = 0; v < 4; ++v) {
+        const float4 a = *reinterpret_cast<const float4*>(p + 4 * v);
+        rin[4 * v] = a.x;
+        rin[4 * v + 1] = a.y;
+        rin[4 * v + 2] = a.z;
+        rin[4 * v + 3] = a.w;
       }
-      rm[q] = v;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int c = cb + q;
+        float v = 0.f;
+        if (n < jb.n && c < c_total) v = c < CA ? lift_in(jb.t[0], n, c) : lift_in(jb.t[1], n, c - CA);
+        rin[q] = v;
+      }
+    }
+    // matrix runs: along c when m_cs == 1, along j when m_rs == 1 (mt)
+    const int j = j0 + (mt ? sc : sr), c = ch * LT_BC + (mt ? sr : sc);
+    const bool run_ok = mt ? (j + 16 <= ds && c < CA) : (j < ds && c + 16 <= CA);
+    if (t0.mvec && run_ok) {
+      const uint16_t* p = t0.m + static_cast<size_t>(j) * t0.m_rs + static_cast<size_t>(c) * t0.m_cs;
+      const uint4 a = *reinterpret_cast<const uint4*>(p), b = *reinterpret_cast<const uint4*>(p + 8);
+      const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        rm[2 * q] = static_cast<uint16_t>(w[q] & 0xFFFFu);
+        rm[2 * q + 1] = static_cast<uint16_t>(w[q] >> 16);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) {
+        const int jq = j0 + (mt ? sc + q : sr), cq = ch * LT_BC + (mt ? sr : sc + q);
+        uint16_t v = 0;
+        if (jq < ds && cq < c_total) {
+          const LiftTerm& t = cq < CA ? jb.t[0] : jb.t[1];
+          const int cl = cq < CA ? cq : cq - CA;
+          v = t.m[static_cast<size_t>(jq) * t.m_rs + static_cast<size_t>(cl) * t.m_cs];
+        }
+        rm[q] = v;
+      }
     }
   };
-  auto store = [&]() {
+  auto pack = [](const uint16_t* h) {
+    return make_uint4(h[0] | (static_cast<uint32_t>(h[1]) << 16), h[2] | (static_cast<uint32_t>(h[3]) << 16),
+                      h[4] | (static_cast<uint32_t>(h[5]) << 16), h[6] | (static_cast<uint32_t>(h[7]) << 16));
+  };
+  auto store = [&](int buf) {
+    uint16_t x[3][16];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = tid + q * 256;
-      s_in[e & (LT_BC - 1)][e >> 5] = rin[q];
+    for (int q = 0; q < 16; ++q) {
+      x[0][q] = bf16_rne(rin[q]);
+      const float r1 = rin[q] - bf16_to_f32(x[0][q]);
+      x[1][q] = bf16_rne(r1);
+      x[2][q] = bf16_rne(r1 - bf16_to_f32(x[1][q]));
     }
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + q * 256;
-      const bool jfast = jb.t[0].m_rs == 1;
-      const int cc = jfast ? (e >> 6) : (e & (LT_BC - 1));
-      const int rr = jfast ? (e & 63) : (e >> 5);
-      s_m[cc][rr] = rm[q];
+    for (int t = 0; t < 3; ++t) {
+      uint4* dst = reinterpret_cast<uint4*>(&s_x[t][buf][sr * LT_ROW + sc]);
+      dst[0] = pack(x[t]);
+      dst[1] = pack(x[t] + 8);
+    }
+    if (mt) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) s_m[buf][(sc + q) * LT_ROW + sr] = rm[q];
+    } else {
+      uint4* dst = reinterpret_cast<uint4*>(&s_m[buf][sr * LT_ROW + sc]);
+      dst[0] = pack(rm);
+      dst[1] = pack(rm + 8);
     }
   };
 
+  floatx4 acc[4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b) acc[b] = floatx4{0.f, 0.f, 0.f, 0.f};
   load(0);
-  store();
+  store(0);
   __syncthreads();
-  for (int c0 = 0; c0 < c_total; c0 += LT_BC) {
-    const bool more = c0 + LT_BC < c_total;
-    if (more) load(c0 + LT_BC);
-#pragma unroll 8
-    for (int cc = 0; cc < LT_BC; ++cc) {
-      const float2 a = *reinterpret_cast<const float2*>(&s_in[cc][tn * 2]);
-      const float4 b = *reinterpret_cast<const float4*>(&s_m[cc][tj * 4]);
-      const float av[2] = {a.x, a.y}, bv[4] = {b.x, b.y, b.z, b.w};
+  for (int ch = 0; ch < nch; ++ch) {
+    const int buf = ch & 1;
+    if (ch + 1 < nch) load(ch + 1);
 #pragma unroll
-      for (int x = 0; x < 2; ++x)
+    for (int kk = 0; kk < LT_BC; kk += 32) {
+      const int koff = kk + (lane >> 4) * 8;
+      const bf16x8 a = *reinterpret_cast<const bf16x8*>(&s_m[buf][(wave * 16 + (lane & 15)) * LT_ROW + koff]);
 #pragma unroll
-        for (int y = 0; y < 4; ++y) acc[x][y] += av[x] * bv[y];
+      for (int b = 0; b < 4; ++b) {
+        const int row = (b * 16 + (lane & 15)) * LT_ROW + koff;
+#pragma unroll
+        for (int t = 0; t < 3; ++t) {
+          const bf16x8 x = *reinterpret_cast<const bf16x8*>(&s_x[t][buf][row]);
+          acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, x, acc[b], 0, 0, 0);
+        }
+      }
     }
-    __syncthreads();
-    if (more) store();
+    if (ch + 1 < nch) store(buf ^ 1);
     __syncthreads();
   }
+  // lane holds outputs j = 16 wave + 4 (lane / 16) + q of row 16 b + lane % 16
+  const int jq = j0 + wave * 16 + (lane >> 4) * 4;
 #pragma unroll
-  for (int x = 0; x < 2; ++x) {
-    const int n = n0 + tn * 2 + x;
+  for (int b = 0; b < 4; ++b) {
+    const int n = n0 + b * 16 + (lane & 15);
     if (n >= jb.n) continue;
-    float* o = jb.out + static_cast<size_t>(n / jb.grp) * jb.blk + static_cast<size_t>(n % jb.grp) * jb.vs;
+    float* o = out_row(n);
 #pragma unroll
-    for (int y = 0; y < 4; ++y) {
-      const int j = j0 + tj * 4 + y;
-      if (j < ds) o[j] = acc[x][y];
+    for (int q = 0; q < 4; ++q) {
+      const int j = jq + q;
+      if (j < ds) o[j] = acc[b][q];
       else if (j < jend) o[j] = 0.f;
     }
   }
@@ -955,12 +1017,16 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   LiftJobs lj{};
   lj.ds = ds;
   const float* PEa = F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj;
-  auto fterm = [](const float* in, int C, const uint16_t* m, int m_rs, int m_cs) {
-    return LiftTerm{in, 0, C, 1, 0, C, m, m_rs, m_cs};
+  // fp32 inputs: the projections, their split-K slices already summed
+  auto fterm = [&](const float* in, int C, const uint16_t* m, int m_rs, int m_cs) {
+    const bool a16 = (reinterpret_cast<uintptr_t>(in) & 15u) == 0 && C % 4 == 0;
+    const bool m16 = (reinterpret_cast<uintptr_t>(m) & 15u) == 0 &&
+                     (m_cs == 1 ? m_rs % 8 == 0 : m_rs == 1 && m_cs % 8 == 0);
+    return LiftTerm{in, 0, C, 1, 0, C, m, m_rs, m_cs, a16 ? 1 : 0, m16 ? 1 : 0};
   };
-  const LiftTerm none{nullptr, 0, 0, 0, 0, 0, nullptr, 0, 0};
-  const LiftTerm posz{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1};
-  const LiftTerm posh{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1};
+  const LiftTerm none{nullptr, 0, 0, 0, 0, 0, nullptr, 0, 0, 0, 0};
+  const LiftTerm posz{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1, 0, 0};
+  const LiftTerm posh{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1, 0, 0};
   const size_t vds = static_cast<size_t>(ds);
   lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, NC, SB + (2 + K) * vsz, K, blk, vsz};
   lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, NC, SB + (2 + 2 * K) * vsz, K, blk, vsz};
@@ -970,10 +1036,11 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, B, F(lay.TZA), 1, vds, vds};
   lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, B, F(lay.THA), 1, vds, vds};
   // feature maps W_z[:, feat] P_phi and W_h[:, feat] P_phi as [5, ds]: input row f is column f of P_phi
-  lj.job[7] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1}, none}, 5, F(lay.FZ), 1, vds, vds};
-  lj.job[8] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1}, none}, 5, F(lay.FH), 1, vds, vds};
+  lj.job[7] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1, 0, 0}, none}, 5, F(lay.FZ), 1, vds, vds};
+  lj.job[8] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1, 0, 0}, none}, 5, F(lay.FH), 1, vds, vds};
   const int lift_cols = static_cast<int>(vsz > vds ? vsz : vds);
-  hipLaunchKernelGGL(lift_kernel, dim3((NC + LT_BN - 1) / LT_BN, (lift_cols + LT_BJ - 1) / LT_BJ, kMaxLiftJobs),
+  const int lift_rows = NC > 2 * B ? NC : 2 * B;
+  hipLaunchKernelGGL(lift_kernel, dim3((lift_rows + LT_BN - 1) / LT_BN, (lift_cols + LT_BJ - 1) / LT_BJ, kMaxLiftJobs),
                      dim3(256), 0, s, lj);
 
   ScanArgs sa{};
