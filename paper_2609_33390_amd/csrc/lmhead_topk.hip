@@ -293,17 +293,51 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   }
 }
 
-// One workgroup per row: every thread folds a strided share of the row's
-// partial keys into a private list, then the lists are merged pairwise through
-// LDS; thread 0's list is the row's ordered top-KP.
+// One workgroup per row: every lane folds a strided share of the row's
+// partial keys into a private sorted list, then the lists meet in butterflies
+// (inside each wavefront, then across the four wavefronts through LDS).  At
+// each level a lane and its partner hold sorted lists a and b; c_j =
+// max(a_j, b_{KP-1-j}) is a bitonic sequence holding the KP largest keys of
+// both, and a bitonic half-cleaner network sorts it, so both lanes leave the
+// level with the same merged list.
+__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
+  const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), m, kWave);
+  const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), m, kWave);
+  return (static_cast<uint64_t>(hi) << 32) | lo;
+}
+
+template <int KP>
+__device__ __forceinline__ void butterfly_merge(uint64_t (&list)[KP], int m) {
+  uint64_t c[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) {
+    const uint64_t o = shfl_xor_u64(list[KP - 1 - j], m);
+    c[j] = list[j] > o ? list[j] : o;
+  }
+#pragma unroll
+  for (int s = KP / 2; s >= 1; s >>= 1) {
+#pragma unroll
+    for (int i = 0; i < KP; ++i) {
+      if ((i & s) == 0) {
+        const uint64_t hi = c[i] > c[i + s] ? c[i] : c[i + s];
+        const uint64_t lo = c[i] > c[i + s] ? c[i + s] : c[i];
+        c[i] = hi;
+        c[i + s] = lo;
+      }
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < KP; ++j) list[j] = c[j];
+}
+
 template <int KP>
 __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restrict__ partial,
                                                          int rows, int n_keys, int K,
                                                          float* __restrict__ cand_logit,
                                                          int32_t* __restrict__ cand_id) {
-  constexpr int NT = 256, BATCH = 4;
-  __shared__ uint64_t sk[KP * NT];
-  const int tid = threadIdx.x;
+  constexpr int NT = 256, NW = NT / kWave, BATCH = 8;
+  __shared__ uint64_t sk[NW][KP];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = blockIdx.x;
   const uint64_t* src = partial + static_cast<size_t>(row) * n_keys;
   uint64_t list[KP];
@@ -321,24 +355,26 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
       if (kb[q] > list[KP - 1]) list_insert(list, kb[q]);
   }
 #pragma unroll
-  for (int j = 0; j < KP; ++j) sk[j * NT + tid] = list[j];
-  __syncthreads();
-  for (int s = NT / 2; s >= 1; s >>= 1) {
-    if (tid < s) {
+  for (int m = 1; m < kWave; m <<= 1) butterfly_merge(list, m);
+  if (lane == 0) {
 #pragma unroll
-      for (int j = 0; j < KP; ++j) {
-        const uint64_t key = sk[j * NT + tid + s];
-        if (key > list[KP - 1]) list_insert(list, key);
-      }
-#pragma unroll
-      for (int j = 0; j < KP; ++j) sk[j * NT + tid] = list[j];
-    }
-    __syncthreads();
+    for (int j = 0; j < KP; ++j) sk[wave][j] = list[j];
   }
-  if (tid < K) {
-    const uint64_t key = sk[tid * NT];
-    cand_logit[static_cast<size_t>(row) * K + tid] = key_logit(key);
-    cand_id[static_cast<size_t>(row) * K + tid] = key_id(key);
+  __syncthreads();
+  if (wave != 0) return;
+  // lane l < NW takes wave l's list; two more levels leave the row's list in lane 0
+#pragma unroll
+  for (int j = 0; j < KP; ++j) list[j] = lane < NW ? sk[lane][j] : 0ull;
+#pragma unroll
+  for (int m = 1; m < NW; m <<= 1) butterfly_merge(list, m);
+  if (lane == 0) {
+#pragma unroll
+    for (int j = 0; j < KP; ++j) {
+      if (j < K) {
+        cand_logit[static_cast<size_t>(row) * K + j] = key_logit(list[j]);
+        cand_id[static_cast<size_t>(row) * K + j] = key_id(list[j]);
+      }
+    }
   }
 }
 
