@@ -87,6 +87,27 @@ def cpu_baseline(blk, budget_s):
                       f"verify, {spent:.1f} s); float64 numpy, host has {os.cpu_count()} logical CPUs"}
 
 
+def time_accept_profile(brisk, dev, M, n_blocks=1 << 20, reps=50):
+    """brisk_accept_profile over n_blocks accepted-prefix lengths (the
+    statistics that feed the position weights), timed with HIP events."""
+    import torch
+
+    g = torch.Generator(device=dev).manual_seed(0)
+    lens = torch.randint(0, M + 1, (n_blocks,), generator=g, device=dev, dtype=torch.int32)
+    for _ in range(3):
+        brisk.accept_profile(lens, M)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        brisk.accept_profile(lens, M)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / reps
+    return {"n_blocks": n_blocks, "M": M, "us_per_call": round(us, 2),
+            "read_GB_per_s": round(4 * n_blocks / (us * 1e-6) / 1e9, 1)}
+
+
 def copy_calibration(n_bytes=1 << 30, reps=3):
     """A plain streaming kernel of known size (read n_bytes, write n_bytes),
     run so that HBM byte counters can be scaled against it."""
@@ -240,6 +261,7 @@ def main():
 
     torch.cuda.synchronize()
     hist = torch.bincount(acc.long(), minlength=wl.L + 1).cpu().tolist()
+    prof = time_accept_profile(brisk, dev, wl.L)
     res = {
         "metric": METRIC, "value": round(value, 1), "unit": "block positions/s", "n_gpus": 1,
         "steps": n, "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
@@ -251,6 +273,7 @@ def main():
         "stages_ms": {"propose": round(statistics.mean(prop_ms), 5),
                       "rerank+verify": round(statistics.mean(rest_ms), 5) if not args.graph else None},
         "accept_hist": hist,
+        "accept_profile": prof,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(blk, args.cpu_budget_s)

@@ -167,6 +167,37 @@ int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_
 int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,
                         int32_t* accept_len, int32_t* correction, void* stream);
 
+/* Workspace bytes brisk_accept_profile needs (written to *bytes). */
+int brisk_accept_profile_workspace_size(int32_t n_blocks, int32_t M, size_t* bytes);
+
+/*
+ * Acceptance profile and efficiency statistics of verified blocks (Section
+ * 3.2 Eq. nonuniform_tpf and Eq. brisk_weighting; Appendix "Brisk Backbone",
+ * Eq. idlm_tpf_instantiation and the rejection-rate estimate of a_i).  From
+ * the accepted-prefix lengths of n_blocks blocks of M proposal positions
+ * (block b reaches positions 1..L_b + 1 and is rejected at L_b + 1 when
+ * L_b < M):
+ *   a[i]      = 1 - rejected_i / reached_i   (1 for a position no block reaches)
+ *   w_raw[i]  = -dFPT/dz_i, z_i = log(a_i / (1 - a_i)), FPT = 1 / TPF with the
+ *               ISD instantiation TPF = (2 + sum_{k=1}^{M-1} A_k) / (2 - A_M),
+ *               A_k = prod_{j<=k} a_j
+ *   w[i]      = M w_raw[i] / (sum_j w_raw[j] + eps)
+ *   tpf_fpt   = {TPF, FPT}
+ *
+ *   accept_len  [n_blocks] int32   accepted-prefix lengths (e.g. the output of
+ *                                  brisk_verify_accept); values outside [0, M]
+ *                                  are clamped into it; may be NULL when
+ *                                  n_blocks == 0
+ *   a, w_raw, w [M] fp64 out;  tpf_fpt [2] fp64 out
+ *   ws          device scratch of brisk_accept_profile_workspace_size bytes
+ *
+ * Limits: 1 <= M <= 1024, 0 <= n_blocks <= 2^30.  Deterministic: the counts
+ * are integers and every floating-point sum runs in a fixed order.
+ */
+int brisk_accept_profile(const int32_t* accept_len, int32_t n_blocks, int32_t M, double eps,
+                         double* a, double* w_raw, double* w, double* tpf_fpt,
+                         void* ws, size_t ws_bytes, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -10,7 +10,9 @@ Entry points (same names as the C ABI):
 
 * :func:`propose_block` - LM-head logits and ordered top-K candidates;
 * :func:`rerank` - the prefix-conditioned corrector over the candidates;
-* :func:`verify_accept` - greedy verification: accept length and correction.
+* :func:`verify_accept` - greedy verification: accept length and correction;
+* :func:`accept_profile` - acceptance profile, tokens per forward and the
+  risk-reward position weights from many blocks' accept lengths.
 """
 from __future__ import annotations
 
@@ -21,13 +23,13 @@ from typing import Dict, Optional, Tuple
 
 import torch
 
-__all__ = ["BriskError", "Corrector", "propose_block", "rerank", "verify_accept", "lib",
-           "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
+__all__ = ["BriskError", "Corrector", "propose_block", "rerank", "verify_accept", "accept_profile",
+           "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
 ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
                "brisk_propose_block", "brisk_rerank_workspace_size", "brisk_rerank",
-               "brisk_verify_accept")
+               "brisk_verify_accept", "brisk_accept_profile_workspace_size", "brisk_accept_profile")
 PSI_FIELDS = ("A_h", "A_e", "P_h", "P_e", "pos_emb", "P_phi", "W_z", "W_h", "W_s", "W_c", "w_g")
 
 _p = ctypes.c_void_p
@@ -78,6 +80,11 @@ def lib() -> ctypes.CDLL:
                                        _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _sz, _p]
             L.brisk_verify_accept.restype = ctypes.c_int
             L.brisk_verify_accept.argtypes = [_p, _p, _i32, _i32, _p, _p, _p]
+            L.brisk_accept_profile_workspace_size.restype = ctypes.c_int
+            L.brisk_accept_profile_workspace_size.argtypes = [_i32, _i32, ctypes.POINTER(_sz)]
+            L.brisk_accept_profile.restype = ctypes.c_int
+            L.brisk_accept_profile.argtypes = [_p, _i32, _i32, ctypes.c_double, _p, _p, _p, _p, _p,
+                                               _sz, _p]
             _lib = L
         return _lib
 
@@ -262,3 +269,25 @@ def verify_accept(proposal: torch.Tensor, verifier: torch.Tensor, *,
                                    _ptr(correction), _stream_ptr(dev, stream))
     _check(st, "brisk_verify_accept")
     return accept_len, correction
+
+
+def accept_profile(accept_len: torch.Tensor, M: int, *, eps: float = 0.0,
+                   workspace: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
+    """Acceptance profile of verified blocks: ``a``, ``w_raw``, ``w`` [M] and
+    ``tpf_fpt`` [2], all float64 on the device of ``accept_len``."""
+    _dev_tensor(accept_len, "accept_len", torch.int32, 1)
+    n = accept_len.shape[0]
+    dev = accept_len.device
+    nbytes = _sz(0)
+    _check(lib().brisk_accept_profile_workspace_size(n, M, ctypes.byref(nbytes)),
+           "brisk_accept_profile_workspace_size")
+    if workspace is None:
+        workspace = _workspace(dev, nbytes.value, "profile")
+    out = {k: torch.empty(M, dtype=torch.float64, device=dev) for k in ("a", "w_raw", "w")}
+    out["tpf_fpt"] = torch.empty(2, dtype=torch.float64, device=dev)
+    st = lib().brisk_accept_profile(_ptr(accept_len) if n > 0 else None, n, M, float(eps),
+                                    _ptr(out["a"]), _ptr(out["w_raw"]), _ptr(out["w"]),
+                                    _ptr(out["tpf_fpt"]), _ptr(workspace), workspace.numel(),
+                                    _stream_ptr(dev, stream))
+    _check(st, "brisk_accept_profile")
+    return out

@@ -10,13 +10,17 @@
 
 namespace {
 
-constexpr int kAbiVersion = 1;
+constexpr int kAbiVersion = 2;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 bool aligned2(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 1u) == 0; }
+bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
+
+constexpr int32_t kMaxProfileM = 1024;
+constexpr int32_t kMaxProfileBlocks = 1 << 30;
 
 int propose_check(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
                   int32_t V, int32_t K, const float* cand_logit, const int32_t* cand_id) {
@@ -148,6 +152,28 @@ int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_
     return BRISK_ERR_UNSUPPORTED;
   brisk::launch_verify(proposal, verifier, B, L, accept_len, correction,
                        static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_accept_profile_workspace_size(int32_t n_blocks, int32_t M, size_t* bytes) {
+  if (!bytes) return BRISK_ERR_NULL;
+  if (M < 1 || M > kMaxProfileM || n_blocks < 0 || n_blocks > kMaxProfileBlocks) return BRISK_ERR_SHAPE;
+  *bytes = brisk::accept_profile_workspace_bytes(n_blocks, M);
+  return BRISK_OK;
+}
+
+int brisk_accept_profile(const int32_t* accept_len, int32_t n_blocks, int32_t M, double eps,
+                         double* a, double* w_raw, double* w, double* tpf_fpt, void* ws,
+                         size_t ws_bytes, void* stream) {
+  if (!a || !w_raw || !w || !tpf_fpt || (n_blocks > 0 && !accept_len)) return BRISK_ERR_NULL;
+  if (M < 1 || M > kMaxProfileM || n_blocks < 0 || n_blocks > kMaxProfileBlocks) return BRISK_ERR_SHAPE;
+  if (!aligned4(accept_len) || !aligned8(a) || !aligned8(w_raw) || !aligned8(w) || !aligned8(tpf_fpt))
+    return BRISK_ERR_UNSUPPORTED;
+  const size_t need = brisk::accept_profile_workspace_bytes(n_blocks, M);
+  if (ws_bytes < need || !ws) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_accept_profile(accept_len, n_blocks, M, eps, a, w_raw, w, tpf_fpt, ws,
+                               static_cast<hipStream_t>(stream));
   return launch_status();
 }
 

@@ -26,4 +26,9 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
 void launch_verify(const int32_t* proposal, const int32_t* verifier, int B, int L,
                    int32_t* accept_len, int32_t* correction, hipStream_t s);
 
+// ---- acceptance profile -------------------------------------------------------
+size_t accept_profile_workspace_bytes(int n_blocks, int M);
+void launch_accept_profile(const int32_t* accept_len, int n_blocks, int M, double eps, double* a,
+                           double* w_raw, double* w, double* tpf_fpt, void* ws, hipStream_t s);
+
 }  // namespace brisk

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 1
+    assert L.brisk_abi_version() == 2
     for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5):
         assert L.brisk_status_str(st).decode()
     assert L.brisk_status_str(123).decode() == "unknown status"
@@ -130,3 +130,28 @@ def test_python_binding_refuses_host_tensors():
         brisk.propose_block(h, h, 4)
     with pytest.raises(ValueError, match="HIP device"):
         brisk.verify_accept(torch.zeros(2, 3, dtype=torch.int32), torch.zeros(2, 3, dtype=torch.int32))
+
+
+@pytest.mark.parametrize("args,want", [
+    ((None, 4, 8, 0.0, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20), ENULL),
+    ((FAKE, 4, 8, 0.0, None, FAKE, FAKE, FAKE, FAKE, 1 << 20), ENULL),
+    ((FAKE, 4, 8, 0.0, FAKE, FAKE, FAKE, None, FAKE, 1 << 20), ENULL),
+    ((FAKE, 4, 0, 0.0, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20), ESHAPE),
+    ((FAKE, 4, 1025, 0.0, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20), ESHAPE),
+    ((FAKE, -1, 8, 0.0, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20), ESHAPE),
+    ((MISALIGNED, 4, 8, 0.0, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 20), EUNSUP),
+    ((FAKE, 4, 8, 0.0, 0x10004, FAKE, FAKE, FAKE, FAKE, 1 << 20), EUNSUP),
+    ((FAKE, 4, 8, 0.0, FAKE, FAKE, FAKE, FAKE, FAKE, 0), EWS),
+    ((FAKE, 4, 8, 0.0, FAKE, FAKE, FAKE, FAKE, None, 1 << 20), EWS),
+])
+def test_accept_profile_validation(args, want):
+    assert brisk.lib().brisk_accept_profile(*args, None) == want
+
+
+def test_accept_profile_workspace_size_query():
+    L = brisk.lib()
+    n = ctypes.c_size_t(0)
+    assert L.brisk_accept_profile_workspace_size(100000, 31, ctypes.byref(n)) == OK and n.value > 0
+    assert L.brisk_accept_profile_workspace_size(0, 31, ctypes.byref(n)) == OK and n.value > 0
+    assert L.brisk_accept_profile_workspace_size(10, 0, ctypes.byref(n)) == ESHAPE
+    assert L.brisk_accept_profile_workspace_size(10, 8, None) == ENULL
