@@ -108,6 +108,40 @@ def time_accept_profile(brisk, dev, M, n_blocks=1 << 20, reps=50):
             "read_GB_per_s": round(4 * n_blocks / (us * 1e-6) / 1e9, 1)}
 
 
+def time_fused_verify(brisk, blk, wl, reps=20):
+    """One LM-head pass over this block's proposal rows plus the previous
+    block's verifier rows (bf16 of the hidden states plus sigma-scaled noise),
+    against two separate passes, timed with HIP events."""
+    import torch
+
+    g = torch.Generator(device=blk.H.device).manual_seed(1)
+    noise = torch.randn(blk.H.shape, generator=g, device=blk.H.device, dtype=torch.float32)
+    Hv = (blk.H.float() + 0.3 * noise).to(torch.bfloat16)
+    both = torch.cat([blk.H, Hv], dim=0).contiguous()
+    rows = wl.B * wl.L
+
+    def fused():
+        brisk.propose_verify(both, blk.W, rows, wl.K)
+
+    def separate():
+        brisk.propose_block(blk.H, blk.W, wl.K)
+        brisk.propose_verify(Hv, blk.W, 0, wl.K)
+
+    out = {"rows": f"{rows} proposal + {rows} verifier"}
+    for name, fn in (("fused_us", fused), ("separate_us", separate)):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        out[name] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
+    return out
+
+
 def copy_calibration(n_bytes=1 << 30, reps=3):
     """A plain streaming kernel of known size (read n_bytes, write n_bytes),
     run so that HBM byte counters can be scaled against it."""
@@ -262,6 +296,7 @@ def main():
     torch.cuda.synchronize()
     hist = torch.bincount(acc.long(), minlength=wl.L + 1).cpu().tolist()
     prof = time_accept_profile(brisk, dev, wl.L)
+    fused = time_fused_verify(brisk, blk, wl)
     res = {
         "metric": METRIC, "value": round(value, 1), "unit": "block positions/s", "n_gpus": 1,
         "steps": n, "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
@@ -274,6 +309,7 @@ def main():
                       "rerank+verify": round(statistics.mean(rest_ms), 5) if not args.graph else None},
         "accept_hist": hist,
         "accept_profile": prof,
+        "propose_verify": fused,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(blk, args.cpu_budget_s)

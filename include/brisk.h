@@ -167,6 +167,50 @@ int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_
 int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,
                         int32_t* accept_len, int32_t* correction, void* stream);
 
+/* Workspace bytes brisk_propose_verify needs (written to *bytes). */
+int brisk_propose_verify_workspace_size(int32_t rows_prop, int32_t rows_ver, int32_t d, int32_t V,
+                                        int32_t K, size_t* bytes);
+
+/*
+ * One LM-head pass for both kinds of rows a self-verifying decoding step
+ * produces (Section 2.1 introspective strided decoding, where proposal and
+ * causal verification come from the same model evaluation; Section 3.3;
+ * Algorithm 1(b) first step and verify): the proposal rows of the next block
+ * get their ordered top-K candidates, exactly as brisk_propose_block, and the
+ * verifier rows of the block under verification get their argmax token (the
+ * largest logit, the lower id on ties), without a second pass over lm_head.
+ *
+ *   hidden      [rows_prop + rows_ver, d] bf16: proposal rows first, then
+ *               verifier rows
+ *   lm_head     [V, d] bf16
+ *   cand_logit, cand_id  [rows_prop, K] out (may be NULL when rows_prop == 0)
+ *   ver_token   [rows_ver] int32 out (may be NULL when rows_ver == 0)
+ *   ws          device scratch of brisk_propose_verify_workspace_size bytes
+ *
+ * Limits as brisk_propose_block with rows = rows_prop + rows_ver >= 1.
+ */
+int brisk_propose_verify(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows_prop,
+                         int32_t rows_ver, int32_t d, int32_t V, int32_t K, float* cand_logit,
+                         int32_t* cand_id, int32_t* ver_token, void* ws, size_t ws_bytes,
+                         void* stream);
+
+/*
+ * Greedy verification and commit (Algorithm 1(b): verify, then commit the
+ * accepted prefix and the correction; Section 2.2 accepted prefix).  For
+ * block b with a = accept length (as brisk_verify_accept):
+ *   committed[b, 0..a-1] = proposal[b, 0..a-1];
+ *   committed[b, a]      = verifier[b, a]        when a < L;
+ *   the rest of the L + 1 slots = -1;  n_committed[b] = a + (a < L).
+ *
+ *   proposal, verifier  [B, L] int32
+ *   accept_len          [B] int32 out, nullable
+ *   committed           [B, L + 1] int32 out
+ *   n_committed         [B] int32 out
+ */
+int brisk_verify_commit(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,
+                        int32_t* accept_len, int32_t* committed, int32_t* n_committed,
+                        void* stream);
+
 /* Workspace bytes brisk_accept_profile needs (written to *bytes). */
 int brisk_accept_profile_workspace_size(int32_t n_blocks, int32_t M, size_t* bytes);
 

@@ -46,7 +46,8 @@ import numpy as np
 
 __all__ = [
     "bf16_to_f64", "lm_logits", "topk", "propose_block", "corrector_init",
-    "confidence_features", "rerank", "verify_accept", "corrector_param_count",
+    "confidence_features", "rerank", "verify_accept", "corrector_param_count", "verifier_argmax",
+    "verify_commit",
 ]
 
 
@@ -209,3 +210,28 @@ def verify_accept(proposal: np.ndarray, verifier: np.ndarray) -> Tuple[np.ndarra
                 correction[b] = verifier[b, i]
                 break
     return accept, correction
+
+
+def verifier_argmax(H_bits: np.ndarray, W_bits: np.ndarray) -> np.ndarray:
+    """The verifier's greedy token of each row: the largest float32 logit, the
+    lower token id among equal ones (the first entry of the ordered top-K)."""
+    _, ids = topk(lm_logits(bf16_to_f64(H_bits), W_bits), 1)
+    return ids[:, 0]
+
+
+def verify_commit(proposal: np.ndarray, verifier: np.ndarray) -> Tuple[np.ndarray, np.ndarray, np.ndarray]:
+    """Committed tokens of each block (Algorithm 1(b) verify and commit): the
+    accepted prefix, then the verifier's token at the first mismatch; the
+    L + 1 slots are padded with -1.  Returns (accept, committed, n_committed)."""
+    B, L = proposal.shape
+    accept, correction = verify_accept(proposal, verifier)
+    committed = np.full((B, L + 1), -1, np.int32)
+    n = np.zeros(B, np.int32)
+    for b in range(B):
+        a = int(accept[b])
+        committed[b, :a] = proposal[b, :a]
+        n[b] = a
+        if a < L:
+            committed[b, a] = correction[b]
+            n[b] = a + 1
+    return accept, committed, n

@@ -11,6 +11,9 @@ Entry points (same names as the C ABI):
 * :func:`propose_block` - LM-head logits and ordered top-K candidates;
 * :func:`rerank` - the prefix-conditioned corrector over the candidates;
 * :func:`verify_accept` - greedy verification: accept length and correction;
+* :func:`propose_verify` - one LM-head pass for proposal rows (top-K) and
+  verifier rows (argmax);
+* :func:`verify_commit` - greedy verification and the committed tokens;
 * :func:`accept_profile` - acceptance profile, tokens per forward and the
   risk-reward position weights from many blocks' accept lengths.
 """
@@ -24,12 +27,14 @@ from typing import Dict, Optional, Tuple
 import torch
 
 __all__ = ["BriskError", "Corrector", "propose_block", "rerank", "verify_accept", "accept_profile",
+           "propose_verify", "verify_commit",
            "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
 ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
                "brisk_propose_block", "brisk_rerank_workspace_size", "brisk_rerank",
-               "brisk_verify_accept", "brisk_accept_profile_workspace_size", "brisk_accept_profile")
+               "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
+               "brisk_verify_commit", "brisk_accept_profile_workspace_size", "brisk_accept_profile")
 PSI_FIELDS = ("A_h", "A_e", "P_h", "P_e", "pos_emb", "P_phi", "W_z", "W_h", "W_s", "W_c", "w_g")
 
 _p = ctypes.c_void_p
@@ -80,6 +85,14 @@ def lib() -> ctypes.CDLL:
                                        _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _sz, _p]
             L.brisk_verify_accept.restype = ctypes.c_int
             L.brisk_verify_accept.argtypes = [_p, _p, _i32, _i32, _p, _p, _p]
+            L.brisk_propose_verify_workspace_size.restype = ctypes.c_int
+            L.brisk_propose_verify_workspace_size.argtypes = [_i32, _i32, _i32, _i32, _i32,
+                                                              ctypes.POINTER(_sz)]
+            L.brisk_propose_verify.restype = ctypes.c_int
+            L.brisk_propose_verify.argtypes = [_p, _p, _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p,
+                                               _sz, _p]
+            L.brisk_verify_commit.restype = ctypes.c_int
+            L.brisk_verify_commit.argtypes = [_p, _p, _i32, _i32, _p, _p, _p, _p]
             L.brisk_accept_profile_workspace_size.restype = ctypes.c_int
             L.brisk_accept_profile_workspace_size.argtypes = [_i32, _i32, ctypes.POINTER(_sz)]
             L.brisk_accept_profile.restype = ctypes.c_int
@@ -291,3 +304,55 @@ def accept_profile(accept_len: torch.Tensor, M: int, *, eps: float = 0.0,
                                     _stream_ptr(dev, stream))
     _check(st, "brisk_accept_profile")
     return out
+
+
+def propose_verify(hidden: torch.Tensor, lm_head: torch.Tensor, rows_prop: int, K: int, *,
+                   cand_logit: Optional[torch.Tensor] = None, cand_id: Optional[torch.Tensor] = None,
+                   ver_token: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                   stream=None) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """One LM-head pass: the first ``rows_prop`` rows of ``hidden`` get ordered
+    top-K candidates, the remaining rows their argmax token.
+    Returns (cand_logit [rows_prop, K], cand_id [rows_prop, K], ver_token [rows_ver])."""
+    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
+    rows, d = hidden.shape
+    V = lm_head.shape[0]
+    rows_ver = rows - rows_prop
+    if rows_prop < 0 or rows_ver < 0:
+        raise ValueError("rows_prop must lie in [0, hidden rows]")
+    dev = hidden.device
+    if cand_logit is None:
+        cand_logit = torch.empty(rows_prop, K, dtype=torch.float32, device=dev)
+    if cand_id is None:
+        cand_id = torch.empty(rows_prop, K, dtype=torch.int32, device=dev)
+    if ver_token is None:
+        ver_token = torch.empty(rows_ver, dtype=torch.int32, device=dev)
+    nbytes = _sz(0)
+    _check(lib().brisk_propose_verify_workspace_size(rows_prop, rows_ver, d, V, K, ctypes.byref(nbytes)),
+           "brisk_propose_verify_workspace_size")
+    ws = workspace if workspace is not None else _workspace(dev, nbytes.value, "propose")
+    st = lib().brisk_propose_verify(_ptr(hidden), _ptr(lm_head), rows_prop, rows_ver, d, V, K,
+                                    _ptr(cand_logit) if rows_prop else None,
+                                    _ptr(cand_id) if rows_prop else None,
+                                    _ptr(ver_token) if rows_ver else None, _ptr(ws), ws.numel(),
+                                    _stream_ptr(dev, stream))
+    _check(st, "brisk_propose_verify")
+    return cand_logit, cand_id, ver_token
+
+
+def verify_commit(proposal: torch.Tensor, verifier: torch.Tensor, *, stream=None
+                  ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
+    """(accept_len [B], committed [B, L + 1] padded with -1, n_committed [B])."""
+    _dev_tensor(proposal, "proposal", torch.int32, 2)
+    _dev_tensor(verifier, "verifier", torch.int32, 2)
+    if proposal.shape != verifier.shape:
+        raise ValueError("proposal and verifier shapes differ")
+    B, L = proposal.shape
+    dev = proposal.device
+    acc = torch.empty(B, dtype=torch.int32, device=dev)
+    committed = torch.empty(B, L + 1, dtype=torch.int32, device=dev)
+    n = torch.empty(B, dtype=torch.int32, device=dev)
+    st = lib().brisk_verify_commit(_ptr(proposal), _ptr(verifier), B, L, _ptr(acc), _ptr(committed),
+                                   _ptr(n), _stream_ptr(dev, stream))
+    _check(st, "brisk_verify_commit")
+    return acc, committed, n

@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 2;
+constexpr int kAbiVersion = 3;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 
@@ -22,18 +22,26 @@ bool aligned8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0
 constexpr int32_t kMaxProfileM = 1024;
 constexpr int32_t kMaxProfileBlocks = 1 << 30;
 
-int propose_check(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
-                  int32_t V, int32_t K, const float* cand_logit, const int32_t* cand_id) {
-  if (!hidden || !lm_head || !cand_logit || !cand_id) return BRISK_ERR_NULL;
+// hidden [rows, d] x lm_head [V, d]: shapes, alignment and the 32-bit byte
+// offsets the LM-head kernel addresses both matrices with
+int lmhead_check(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d, int32_t V,
+                 int32_t K) {
+  if (!hidden || !lm_head) return BRISK_ERR_NULL;
   if (rows < 1 || rows > kMaxRows || d < 8 || d > kMaxD || K < 1 || K > 64 || V < K)
     return BRISK_ERR_SHAPE;
-  if (d % 8 != 0 || !aligned16(hidden) || !aligned16(lm_head) || !aligned4(cand_logit) ||
-      !aligned4(cand_id))
-    return BRISK_ERR_UNSUPPORTED;
-  // the LM-head kernel addresses both matrices with 32-bit byte offsets
+  if (d % 8 != 0 || !aligned16(hidden) || !aligned16(lm_head)) return BRISK_ERR_UNSUPPORTED;
   if (static_cast<uint64_t>(V) * d * 2 >= (uint64_t{1} << 32) ||
       static_cast<uint64_t>(rows) * d * 2 >= (uint64_t{1} << 32))
     return BRISK_ERR_UNSUPPORTED;
+  return BRISK_OK;
+}
+
+int propose_check(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
+                  int32_t V, int32_t K, const float* cand_logit, const int32_t* cand_id) {
+  if (!hidden || !lm_head || !cand_logit || !cand_id) return BRISK_ERR_NULL;
+  const int st = lmhead_check(hidden, lm_head, rows, d, V, K);
+  if (st != BRISK_OK) return st;
+  if (!aligned4(cand_logit) || !aligned4(cand_id)) return BRISK_ERR_UNSUPPORTED;
   return BRISK_OK;
 }
 
@@ -97,7 +105,38 @@ int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head, int32_t
   const size_t need = brisk::propose_workspace_bytes(rows, V, K);
   if (ws_bytes < need || (need > 0 && !ws)) return BRISK_ERR_WORKSPACE;
   if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
-  brisk::launch_propose(hidden, lm_head, rows, d, V, K, cand_logit, cand_id, ws,
+  brisk::launch_propose(hidden, lm_head, rows, d, V, K, rows, cand_logit, cand_id, nullptr, ws,
+                        static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_propose_verify_workspace_size(int32_t rows_prop, int32_t rows_ver, int32_t d, int32_t V,
+                                        int32_t K, size_t* bytes) {
+  if (!bytes) return BRISK_ERR_NULL;
+  const int64_t rows = static_cast<int64_t>(rows_prop) + rows_ver;
+  if (rows_prop < 0 || rows_ver < 0 || rows < 1 || rows > kMaxRows || d < 8 || d > kMaxD || K < 1 ||
+      K > 64 || V < K)
+    return BRISK_ERR_SHAPE;
+  *bytes = brisk::propose_workspace_bytes(static_cast<int>(rows), V, K);
+  return BRISK_OK;
+}
+
+int brisk_propose_verify(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows_prop,
+                         int32_t rows_ver, int32_t d, int32_t V, int32_t K, float* cand_logit,
+                         int32_t* cand_id, int32_t* ver_token, void* ws, size_t ws_bytes,
+                         void* stream) {
+  if (!hidden || !lm_head || (rows_prop > 0 && (!cand_logit || !cand_id)) || (rows_ver > 0 && !ver_token))
+    return BRISK_ERR_NULL;
+  const int64_t rows64 = static_cast<int64_t>(rows_prop) + rows_ver;
+  if (rows_prop < 0 || rows_ver < 0 || rows64 < 1 || rows64 > kMaxRows) return BRISK_ERR_SHAPE;
+  const int32_t rows = static_cast<int32_t>(rows64);
+  const int st = lmhead_check(hidden, lm_head, rows, d, V, K);
+  if (st != BRISK_OK) return st;
+  if (!aligned4(cand_logit) || !aligned4(cand_id) || !aligned4(ver_token)) return BRISK_ERR_UNSUPPORTED;
+  const size_t need = brisk::propose_workspace_bytes(rows, V, K);
+  if (ws_bytes < need || !ws) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_propose(hidden, lm_head, rows, d, V, K, rows_prop, cand_logit, cand_id, ver_token, ws,
                         static_cast<hipStream_t>(stream));
   return launch_status();
 }
@@ -151,6 +190,18 @@ int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_
   if (!aligned4(proposal) || !aligned4(verifier) || !aligned4(accept_len) || !aligned4(correction))
     return BRISK_ERR_UNSUPPORTED;
   brisk::launch_verify(proposal, verifier, B, L, accept_len, correction,
+                       static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_verify_commit(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,
+                        int32_t* accept_len, int32_t* committed, int32_t* n_committed, void* stream) {
+  if (!proposal || !verifier || !committed || !n_committed) return BRISK_ERR_NULL;
+  if (B < 1 || L < 1 || static_cast<int64_t>(B) * (L + 1) > (int64_t{1} << 30)) return BRISK_ERR_SHAPE;
+  if (!aligned4(proposal) || !aligned4(verifier) || !aligned4(accept_len) || !aligned4(committed) ||
+      !aligned4(n_committed))
+    return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_commit(proposal, verifier, B, L, accept_len, committed, n_committed,
                        static_cast<hipStream_t>(stream));
   return launch_status();
 }

@@ -11,8 +11,11 @@ namespace brisk {
 
 // ---- propose: LM head + fused top-K + merge --------------------------------
 size_t propose_workspace_bytes(int rows, int V, int K);
+// rows = proposal rows (K candidates each) followed by verifier rows (argmax
+// each): rows_prop of them are proposal rows.
 void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
-                    float* cand_logit, int32_t* cand_id, void* ws, hipStream_t s);
+                    int rows_prop, float* cand_logit, int32_t* cand_id, int32_t* ver_token,
+                    void* ws, hipStream_t s);
 
 // ---- rerank: hoisted projections + sequential scan -------------------------
 size_t rerank_workspace_bytes(const brisk_corrector& c, int B, int L, int K);
@@ -25,6 +28,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
 // ---- verify -----------------------------------------------------------------
 void launch_verify(const int32_t* proposal, const int32_t* verifier, int B, int L,
                    int32_t* accept_len, int32_t* correction, hipStream_t s);
+void launch_commit(const int32_t* proposal, const int32_t* verifier, int B, int L,
+                   int32_t* accept_len, int32_t* committed, int32_t* n_committed, hipStream_t s);
 
 // ---- acceptance profile -------------------------------------------------------
 size_t accept_profile_workspace_bytes(int n_blocks, int M);

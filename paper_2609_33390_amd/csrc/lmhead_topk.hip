@@ -330,11 +330,14 @@ __device__ __forceinline__ void butterfly_merge(uint64_t (&list)[KP], int m) {
   for (int j = 0; j < KP; ++j) list[j] = c[j];
 }
 
+// Rows below rows_prop are proposal rows (K candidates out); the rows after
+// them are verifier rows, whose argmax (the top key) goes to ver_token.
 template <int KP>
 __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restrict__ partial,
-                                                         int rows, int n_keys, int K,
+                                                         int rows, int n_keys, int K, int rows_prop,
                                                          float* __restrict__ cand_logit,
-                                                         int32_t* __restrict__ cand_id) {
+                                                         int32_t* __restrict__ cand_id,
+                                                         int32_t* __restrict__ ver_token) {
   constexpr int NT = 256, NW = NT / kWave, BATCH = 8;
   __shared__ uint64_t sk[NW][KP];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -368,11 +371,15 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
 #pragma unroll
   for (int m = 1; m < NW; m <<= 1) butterfly_merge(list, m);
   if (lane == 0) {
+    if (row >= rows_prop) {
+      ver_token[row - rows_prop] = key_id(list[0]);
+    } else {
 #pragma unroll
-    for (int j = 0; j < KP; ++j) {
-      if (j < K) {
-        cand_logit[static_cast<size_t>(row) * K + j] = key_logit(list[j]);
-        cand_id[static_cast<size_t>(row) * K + j] = key_id(list[j]);
+      for (int j = 0; j < KP; ++j) {
+        if (j < K) {
+          cand_logit[static_cast<size_t>(row) * K + j] = key_logit(list[j]);
+          cand_id[static_cast<size_t>(row) * K + j] = key_id(list[j]);
+        }
       }
     }
   }
@@ -425,14 +432,15 @@ void launch_tile(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, 
 
 template <int KP>
 void launch_kp(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
-               uint64_t* partial, float* cand_logit, int32_t* cand_id, hipStream_t s) {
+               int rows_prop, uint64_t* partial, float* cand_logit, int32_t* cand_id,
+               int32_t* ver_token, hipStream_t s) {
   switch (p.cfg) {
     case 0: launch_tile<SmallRows, KP>(p, H, W, rows, d, V, partial, s); break;
     case 1: launch_tile<MidRows, KP>(p, H, W, rows, d, V, partial, s); break;
     default: launch_tile<LargeRows, KP>(p, H, W, rows, d, V, partial, s); break;
   }
   hipLaunchKernelGGL((topk_merge_kernel<KP>), dim3(rows), dim3(256), 0, s, partial, rows,
-                     p.n_parts * KP, K, cand_logit, cand_id);
+                     p.n_parts * KP, K, rows_prop, cand_logit, cand_id, ver_token);
 }
 
 }  // namespace
@@ -443,15 +451,16 @@ size_t propose_workspace_bytes(int rows, int V, int K) {
 }
 
 void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
-                    float* cand_logit, int32_t* cand_id, void* ws, hipStream_t s) {
+                    int rows_prop, float* cand_logit, int32_t* cand_id, int32_t* ver_token,
+                    void* ws, hipStream_t s) {
   const Plan p = make_plan(rows, V, K);
   uint64_t* partial = static_cast<uint64_t*>(ws);
   switch (p.KP) {
-    case 4: launch_kp<4>(p, H, W, rows, d, V, K, partial, cand_logit, cand_id, s); break;
-    case 8: launch_kp<8>(p, H, W, rows, d, V, K, partial, cand_logit, cand_id, s); break;
-    case 16: launch_kp<16>(p, H, W, rows, d, V, K, partial, cand_logit, cand_id, s); break;
-    case 32: launch_kp<32>(p, H, W, rows, d, V, K, partial, cand_logit, cand_id, s); break;
-    default: launch_kp<64>(p, H, W, rows, d, V, K, partial, cand_logit, cand_id, s); break;
+    case 4: launch_kp<4>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    case 8: launch_kp<8>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    case 16: launch_kp<16>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    case 32: launch_kp<32>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    default: launch_kp<64>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
   }
 }
 

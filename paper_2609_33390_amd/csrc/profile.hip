@@ -33,20 +33,55 @@ int hist_groups(int n_blocks) {
 __global__ __launch_bounds__(kHistThreads) void accept_hist_kernel(const int32_t* __restrict__ len,
                                                                    int n_blocks, int M,
                                                                    uint32_t* __restrict__ part) {
-  extern __shared__ uint32_t h[];  // M + 1 bins
-  for (int j = threadIdx.x; j <= M; j += kHistThreads) h[j] = 0;
+  // M < 64: every thread owns a private column of counters (no atomics, no
+  // conflicting updates); otherwise one shared histogram with LDS atomics
+  extern __shared__ uint32_t h[];
+  const bool priv = M < kWave;
+  const int cols = priv ? kHistThreads : 1;
+  for (int j = threadIdx.x; j < (M + 1) * cols; j += kHistThreads) h[j] = 0;
   __syncthreads();
   const int per = (n_blocks + gridDim.x - 1) / gridDim.x;
   const int b0 = blockIdx.x * per;
   const int b1 = min(b0 + per, n_blocks);
-  for (int b = b0 + threadIdx.x; b < b1; b += kHistThreads) {
-    int L = len[b];
-    L = L < 0 ? 0 : (L > M ? M : L);
-    atomicAdd(&h[L], 1u);
+  constexpr int BATCH = 8;
+  for (int bb = b0; bb < b1; bb += kHistThreads * BATCH) {
+    int Ls[BATCH];
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q) {
+      const int b = bb + q * kHistThreads + threadIdx.x;
+      Ls[q] = b < b1 ? len[b] : -1;
+    }
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q) {
+      const int b = bb + q * kHistThreads + threadIdx.x;
+      if (b >= b1) continue;
+      const int L = Ls[q] < 0 ? 0 : (Ls[q] > M ? M : Ls[q]);
+      if (priv) h[L * kHistThreads + threadIdx.x] += 1u;
+      else atomicAdd(&h[L], 1u);
+    }
   }
   __syncthreads();
-  for (int j = threadIdx.x; j <= M; j += kHistThreads)
-    part[static_cast<size_t>(blockIdx.x) * (M + 1) + j] = h[j];
+  if (priv) {
+    // bin j: sum of the 256 private counters (each thread adds its row of 4)
+    for (int j = 0; j <= M; ++j) {
+      uint32_t v = h[j * kHistThreads + threadIdx.x];
+      v += __shfl_xor(v, 1, kWave);
+      v += __shfl_xor(v, 2, kWave);
+      v += __shfl_xor(v, 4, kWave);
+      v += __shfl_xor(v, 8, kWave);
+      v += __shfl_xor(v, 16, kWave);
+      v += __shfl_xor(v, 32, kWave);
+      __syncthreads();
+      if ((threadIdx.x & 63) == 0) h[j * kHistThreads + threadIdx.x] = v;  // wave totals in place
+      __syncthreads();
+      if (threadIdx.x == 0)
+        part[static_cast<size_t>(blockIdx.x) * (M + 1) + j] =
+            h[j * kHistThreads] + h[j * kHistThreads + 64] + h[j * kHistThreads + 128] + h[j * kHistThreads + 192];
+    }
+  } else {
+    for (int j = threadIdx.x; j <= M; j += kHistThreads)
+      part[static_cast<size_t>(blockIdx.x) * (M + 1) + j] = h[j];
+  }
 }
 
 __global__ __launch_bounds__(kHistThreads) void accept_profile_kernel(const uint32_t* __restrict__ part,
@@ -57,16 +92,33 @@ __global__ __launch_bounds__(kHistThreads) void accept_profile_kernel(const uint
                                                                       double* __restrict__ tpf_fpt) {
   extern __shared__ double sm[];
   double* cnt = sm;              // [M + 1] block counts per accepted length
+  __shared__ uint32_t c32[1025];
   double* a = cnt + (M + 1);     // [M]
   double* A = a + M;             // [M + 1] survival
   double* S = A + (M + 1);       // [M + 1] S_i = sum_{k=i}^{M-1} A_k
   double* R = S + (M + 1);       // [M] raw sensitivities
   __shared__ double s_num, s_den, s_sum;
-  for (int j = threadIdx.x; j <= M; j += kHistThreads) {
-    uint64_t c = 0;
-    for (int g = 0; g < groups; ++g) c += part[static_cast<size_t>(g) * (M + 1) + j];
-    cnt[j] = static_cast<double>(c);
+  // add the partial histograms: every (group, length) entry is one load, a
+  // batch of loads in flight per thread, integer LDS atomics (order-free)
+  for (int j = threadIdx.x; j <= M; j += kHistThreads) c32[j] = 0;
+  __syncthreads();
+  const int n_ent = groups * (M + 1);
+  constexpr int BATCH = 8;
+  for (int e0 = 0; e0 < n_ent; e0 += kHistThreads * BATCH) {
+    uint32_t v[BATCH];
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q) {
+      const int e = e0 + q * kHistThreads + threadIdx.x;
+      v[q] = e < n_ent ? part[e] : 0u;
+    }
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q) {
+      const int e = e0 + q * kHistThreads + threadIdx.x;
+      if (e < n_ent && v[q]) atomicAdd(&c32[e % (M + 1)], v[q]);
+    }
   }
+  __syncthreads();
+  for (int j = threadIdx.x; j <= M; j += kHistThreads) cnt[j] = static_cast<double>(c32[j]);
   __syncthreads();
   if (threadIdx.x == 0) {
     // reached_i = #{L >= i-1}, rejected_i = #{L = i-1}
@@ -117,7 +169,8 @@ void launch_accept_profile(const int32_t* accept_len, int n_blocks, int M, doubl
                            double* w_raw, double* w, double* tpf_fpt, void* ws, hipStream_t s) {
   const int groups = hist_groups(n_blocks);
   uint32_t* part = static_cast<uint32_t*>(ws);
-  hipLaunchKernelGGL(accept_hist_kernel, dim3(groups), dim3(kHistThreads), (M + 1) * sizeof(uint32_t), s,
+  const size_t hist_lds = (M + 1) * sizeof(uint32_t) * (M < kWave ? kHistThreads : 1);
+  hipLaunchKernelGGL(accept_hist_kernel, dim3(groups), dim3(kHistThreads), hist_lds, s,
                      accept_len, n_blocks, M, part);
   hipLaunchKernelGGL(accept_profile_kernel, dim3(1), dim3(kHistThreads), (5 * M + 3) * sizeof(double), s,
                      part, groups, M, eps, a, w_raw, w, tpf_fpt);

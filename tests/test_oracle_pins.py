@@ -329,3 +329,32 @@ def test_unique_self_consistent_path_is_the_greedy_one():
     assert np.array_equal(tok[consistent][0], free["selected"][0])
     # the corrector changed at least one choice, so the check is not vacuous
     assert not np.array_equal(free["selected"][0], ci[:, 0])
+
+
+def test_verify_commit_brute_force_and_invariants():
+    rng = np.random.default_rng(11)
+    for L in (1, 2, 5, 9):
+        for _ in range(40):
+            prop = rng.integers(0, 3, (3, L)).astype(np.int32)
+            ver = rng.integers(0, 3, (3, L)).astype(np.int32)
+            acc, com, n = oracle.verify_commit(prop, ver)
+            for b in range(3):
+                a = next((i for i in range(L) if prop[b, i] != ver[b, i]), L)
+                want = list(prop[b, :a]) + ([int(ver[b, a])] if a < L else [])
+                assert acc[b] == a and n[b] == len(want)
+                assert list(com[b, :n[b]]) == want and np.all(com[b, n[b]:] == -1)
+                # every committed token is what the verifier would emit at its position
+                assert np.array_equal(com[b, :n[b]], ver[b, :n[b]])
+
+
+def test_verifier_argmax_ties_and_planted_row():
+    H = np.zeros((2, 8), np.float32)
+    H[:, 0] = 1.0
+    W = np.zeros((6, 8), np.float32)
+    W[2, 0] = 2.0
+    W[4, 0] = 2.0            # exact tie with row 2: the lower id wins
+    W[5, 0] = -3.0
+    bits = lambda x: (np.asarray(x, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+    assert list(oracle.verifier_argmax(bits(H), bits(W))) == [2, 2]
+    H[1, 0] = -1.0           # now row 5 (-3 * -1 = 3) is the largest
+    assert list(oracle.verifier_argmax(bits(H), bits(W))) == [2, 5]
