@@ -142,6 +142,27 @@ def time_fused_verify(brisk, blk, wl, reps=20):
     return out
 
 
+def time_corrector_loss(brisk, blk, wl, corr, cl, ci, acc, reps=50):
+    """brisk_corrector_loss on this step's candidates, refined logits and
+    accept lengths, with verifier rows = bf16(hidden + 0.3 noise)."""
+    import torch
+
+    rr = brisk.rerank(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, wl.B, wl.L, want_scores=True)
+    g = torch.Generator(device=blk.H.device).manual_seed(2)
+    Hv = (blk.H.float() + 0.3 * torch.randn(blk.H.shape, generator=g, device=blk.H.device)).to(torch.bfloat16)
+    fn = lambda: brisk.corrector_loss(Hv, blk.W, ci, cl, rr["refined"], acc, wl.B, wl.L)
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return {"positions": wl.B * wl.L, "us_per_call": round(e0.elapsed_time(e1) * 1e3 / reps, 2)}
+
+
 def copy_calibration(n_bytes=1 << 30, reps=3):
     """A plain streaming kernel of known size (read n_bytes, write n_bytes),
     run so that HBM byte counters can be scaled against it."""
@@ -297,6 +318,7 @@ def main():
     hist = torch.bincount(acc.long(), minlength=wl.L + 1).cpu().tolist()
     prof = time_accept_profile(brisk, dev, wl.L)
     fused = time_fused_verify(brisk, blk, wl)
+    loss = time_corrector_loss(brisk, blk, wl, corr, cl, ci, acc)
     res = {
         "metric": METRIC, "value": round(value, 1), "unit": "block positions/s", "n_gpus": 1,
         "steps": n, "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
@@ -310,6 +332,7 @@ def main():
         "accept_hist": hist,
         "accept_profile": prof,
         "propose_verify": fused,
+        "corrector_loss": loss,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(blk, args.cpu_budget_s)

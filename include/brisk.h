@@ -211,6 +211,34 @@ int brisk_verify_commit(const int32_t* proposal, const int32_t* verifier, int32_
                         int32_t* accept_len, int32_t* committed, int32_t* n_committed,
                         void* stream);
 
+/*
+ * Corrector training loss, forward (Appendix "Candidate-Refinement Head
+ * Details", Eq. head_training_loss).  For position j of block b (row
+ * r = b * L + j) with candidates v_{r,k}:
+ *   p_S = softmax_k <lm_head[v_{r,k}], ver_hidden[r]>   (verifier, restricted)
+ *   q_S = softmax_k cand_logit[r, k]                     (base proposal, restricted)
+ *   r   = softmax_k refined[r, k]                        (corrector)
+ *   loss_pos[r] = CE(p_S, r) + beta * KL(q_S || r)  on reached positions
+ *                 (j <= accept_len[b]: the accepted prefix and the first
+ *                 rejection), 0 elsewhere
+ *   loss_mean   = {mean of loss_pos over reached positions, their count}
+ *
+ *   ver_hidden  [B*L, d] bf16   the verifier's hidden states
+ *   lm_head     [V, d]   bf16
+ *   cand_id, cand_logit, refined  [B*L, K] (from brisk_propose_block and
+ *               brisk_rerank)
+ *   accept_len  [B] int32      (from brisk_verify_accept)
+ *   loss_pos    [B*L] fp32 out;  ce, kl [B*L] fp32 out, nullable
+ *   loss_mean   [2]   fp32 out
+ *
+ * Limits: 1 <= K <= 64, d % 8 == 0 with 16-byte aligned bf16 pointers, B*L
+ * <= 2^20.  Deterministic (fixed-order sums).
+ */
+int brisk_corrector_loss(const uint16_t* ver_hidden, const uint16_t* lm_head, const int32_t* cand_id,
+                         const float* cand_logit, const float* refined, const int32_t* accept_len,
+                         int32_t B, int32_t L, int32_t K, int32_t d, int32_t V, float beta,
+                         float* loss_pos, float* ce, float* kl, float* loss_mean, void* stream);
+
 /* Workspace bytes brisk_accept_profile needs (written to *bytes). */
 int brisk_accept_profile_workspace_size(int32_t n_blocks, int32_t M, size_t* bytes);
 

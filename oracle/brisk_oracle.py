@@ -47,7 +47,7 @@ import numpy as np
 __all__ = [
     "bf16_to_f64", "lm_logits", "topk", "propose_block", "corrector_init",
     "confidence_features", "rerank", "verify_accept", "corrector_param_count", "verifier_argmax",
-    "verify_commit",
+    "verify_commit", "reached_mask", "corrector_loss",
 ]
 
 
@@ -235,3 +235,49 @@ def verify_commit(proposal: np.ndarray, verifier: np.ndarray) -> Tuple[np.ndarra
             committed[b, a] = correction[b]
             n[b] = a + 1
     return accept, committed, n
+
+
+def reached_mask(accept: np.ndarray, L: int) -> np.ndarray:
+    """Positions whose verification decision is reached (Appendix head
+    details): the accepted prefix and the first rejected position; every
+    position of a fully accepted block.  [B, L] bool."""
+    B = len(accept)
+    m = np.zeros((B, L), dtype=bool)
+    for b in range(B):
+        m[b, :min(int(accept[b]) + 1, L)] = True
+    return m
+
+
+def _log_softmax(x: np.ndarray) -> np.ndarray:
+    x = np.asarray(x, dtype=np.float64)
+    m = x.max(axis=-1, keepdims=True)
+    return x - m - np.log(np.exp(x - m).sum(axis=-1, keepdims=True))
+
+
+def corrector_loss(ver_H: np.ndarray, W_bits: np.ndarray, cand_id: np.ndarray,
+                   cand_logit: np.ndarray, refined: np.ndarray, accept: np.ndarray, L: int,
+                   beta: float = 0.01) -> Dict[str, np.ndarray]:
+    """Corrector training loss on one batch of blocks (Appendix head details,
+    Eq. head_training_loss).
+
+    At position j with candidate set S_j: p_S = the verifier distribution
+    restricted to S_j and renormalised (softmax of the verifier logits
+    <E_out[v], h_j> at the candidate ids), q_S = the base distribution
+    restricted to S_j (softmax of the candidate logits), r = softmax of the
+    refined logits.  l_j = CE(p_S, r) + beta KL(q_S || r); the loss is the
+    mean of l_j over the reached positions.  ``ver_H`` is [B*L, d] float64.
+    """
+    rows, K = cand_id.shape
+    W = bf16_to_f64(W_bits)
+    lp = np.einsum("rkd,rd->rk", W[cand_id.astype(np.int64)], ver_H)
+    log_p = _log_softmax(lp)
+    log_q = _log_softmax(cand_logit)
+    log_r = _log_softmax(refined)
+    p, q = np.exp(log_p), np.exp(log_q)
+    ce = -(p * log_r).sum(axis=1)
+    kl = (q * (log_q - log_r)).sum(axis=1)
+    per = ce + beta * kl
+    mask = reached_mask(accept, L).reshape(rows)
+    loss_pos = np.where(mask, per, 0.0)
+    return dict(loss_pos=loss_pos, ce=ce, kl=kl, mask=mask,
+                mean=float(loss_pos.sum() / mask.sum()), count=int(mask.sum()))

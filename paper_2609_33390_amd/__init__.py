@@ -14,6 +14,7 @@ Entry points (same names as the C ABI):
 * :func:`propose_verify` - one LM-head pass for proposal rows (top-K) and
   verifier rows (argmax);
 * :func:`verify_commit` - greedy verification and the committed tokens;
+* :func:`corrector_loss` - the corrector's training loss on reached positions;
 * :func:`accept_profile` - acceptance profile, tokens per forward and the
   risk-reward position weights from many blocks' accept lengths.
 """
@@ -27,14 +28,15 @@ from typing import Dict, Optional, Tuple
 import torch
 
 __all__ = ["BriskError", "Corrector", "propose_block", "rerank", "verify_accept", "accept_profile",
-           "propose_verify", "verify_commit",
+           "propose_verify", "verify_commit", "corrector_loss",
            "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
 ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
                "brisk_propose_block", "brisk_rerank_workspace_size", "brisk_rerank",
                "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
-               "brisk_verify_commit", "brisk_accept_profile_workspace_size", "brisk_accept_profile")
+               "brisk_verify_commit", "brisk_corrector_loss", "brisk_accept_profile_workspace_size",
+               "brisk_accept_profile")
 PSI_FIELDS = ("A_h", "A_e", "P_h", "P_e", "pos_emb", "P_phi", "W_z", "W_h", "W_s", "W_c", "w_g")
 
 _p = ctypes.c_void_p
@@ -93,6 +95,9 @@ def lib() -> ctypes.CDLL:
                                                _sz, _p]
             L.brisk_verify_commit.restype = ctypes.c_int
             L.brisk_verify_commit.argtypes = [_p, _p, _i32, _i32, _p, _p, _p, _p]
+            L.brisk_corrector_loss.restype = ctypes.c_int
+            L.brisk_corrector_loss.argtypes = [_p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32,
+                                               ctypes.c_float, _p, _p, _p, _p, _p]
             L.brisk_accept_profile_workspace_size.restype = ctypes.c_int
             L.brisk_accept_profile_workspace_size.argtypes = [_i32, _i32, ctypes.POINTER(_sz)]
             L.brisk_accept_profile.restype = ctypes.c_int
@@ -356,3 +361,27 @@ def verify_commit(proposal: torch.Tensor, verifier: torch.Tensor, *, stream=None
                                    _ptr(n), _stream_ptr(dev, stream))
     _check(st, "brisk_verify_commit")
     return acc, committed, n
+
+
+def corrector_loss(ver_hidden: torch.Tensor, lm_head: torch.Tensor, cand_id: torch.Tensor,
+                   cand_logit: torch.Tensor, refined: torch.Tensor, accept_len: torch.Tensor,
+                   B: int, L: int, *, beta: float = 0.01, stream=None) -> Dict[str, torch.Tensor]:
+    """Per-position losses ``loss_pos``, ``ce``, ``kl`` [B*L] and ``loss_mean``
+    [2] = (mean over reached positions, their count)."""
+    _dev_tensor(ver_hidden, "ver_hidden", torch.bfloat16, 2)
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
+    _dev_tensor(refined, "refined", torch.float32, 2)
+    _dev_tensor(accept_len, "accept_len", torch.int32, 1)
+    rows, K = cand_id.shape
+    d, V = ver_hidden.shape[1], lm_head.shape[0]
+    dev = ver_hidden.device
+    out = {k: torch.empty(rows, dtype=torch.float32, device=dev) for k in ("loss_pos", "ce", "kl")}
+    out["loss_mean"] = torch.empty(2, dtype=torch.float32, device=dev)
+    st = lib().brisk_corrector_loss(_ptr(ver_hidden), _ptr(lm_head), _ptr(cand_id), _ptr(cand_logit),
+                                    _ptr(refined), _ptr(accept_len), B, L, K, d, V, float(beta),
+                                    _ptr(out["loss_pos"]), _ptr(out["ce"]), _ptr(out["kl"]),
+                                    _ptr(out["loss_mean"]), _stream_ptr(dev, stream))
+    _check(st, "brisk_corrector_loss")
+    return out

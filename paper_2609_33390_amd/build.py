@@ -17,7 +17,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libbrisk.so")
-SOURCES = ["lmhead_topk.hip", "corrector.hip", "verify.hip", "profile.hip", "brisk_abi.cpp"]
+SOURCES = ["lmhead_topk.hip", "corrector.hip", "verify.hip", "profile.hip", "loss.hip", "brisk_abi.cpp"]
 ARCH = "gfx950"
 # Packed-fp32 instructions stay off: the compiler must not form them itself.
 GPU_FLAGS = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]

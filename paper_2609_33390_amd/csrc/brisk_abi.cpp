@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 3;
+constexpr int kAbiVersion = 4;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 
@@ -203,6 +203,25 @@ int brisk_verify_commit(const int32_t* proposal, const int32_t* verifier, int32_
     return BRISK_ERR_UNSUPPORTED;
   brisk::launch_commit(proposal, verifier, B, L, accept_len, committed, n_committed,
                        static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_corrector_loss(const uint16_t* ver_hidden, const uint16_t* lm_head, const int32_t* cand_id,
+                         const float* cand_logit, const float* refined, const int32_t* accept_len,
+                         int32_t B, int32_t L, int32_t K, int32_t d, int32_t V, float beta,
+                         float* loss_pos, float* ce, float* kl, float* loss_mean, void* stream) {
+  if (!ver_hidden || !lm_head || !cand_id || !cand_logit || !refined || !accept_len || !loss_pos ||
+      !loss_mean)
+    return BRISK_ERR_NULL;
+  if (B < 1 || L < 1 || static_cast<int64_t>(B) * L > kMaxRows || K < 1 || K > 64 || V < K || d < 8 ||
+      d > kMaxD)
+    return BRISK_ERR_SHAPE;
+  if (d % 8 != 0 || !aligned16(ver_hidden) || !aligned16(lm_head) || !aligned4(cand_id) ||
+      !aligned4(cand_logit) || !aligned4(refined) || !aligned4(accept_len) || !aligned4(loss_pos) ||
+      !aligned4(ce) || !aligned4(kl) || !aligned4(loss_mean))
+    return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_corrector_loss(ver_hidden, lm_head, cand_id, cand_logit, refined, accept_len, B, L, K, d,
+                               V, beta, loss_pos, ce, kl, loss_mean, static_cast<hipStream_t>(stream));
   return launch_status();
 }
 

@@ -31,6 +31,12 @@ void launch_verify(const int32_t* proposal, const int32_t* verifier, int B, int 
 void launch_commit(const int32_t* proposal, const int32_t* verifier, int B, int L,
                    int32_t* accept_len, int32_t* committed, int32_t* n_committed, hipStream_t s);
 
+// ---- corrector training loss (forward) ---------------------------------------
+void launch_corrector_loss(const uint16_t* ver_hidden, const uint16_t* lm_head, const int32_t* cand_id,
+                           const float* cand_logit, const float* refined, const int32_t* accept_len,
+                           int B, int L, int K, int d, int V, float beta, float* loss_pos, float* ce,
+                           float* kl, float* loss_mean, hipStream_t s);
+
 // ---- acceptance profile -------------------------------------------------------
 size_t accept_profile_workspace_bytes(int n_blocks, int M);
 void launch_accept_profile(const int32_t* accept_len, int n_blocks, int M, double eps, double* a,

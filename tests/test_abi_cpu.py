@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 3
+    assert L.brisk_abi_version() == 4
     for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5):
         assert L.brisk_status_str(st).decode()
     assert L.brisk_status_str(123).decode() == "unknown status"
@@ -185,3 +185,18 @@ def test_propose_verify_validation(kw, want):
 ])
 def test_verify_commit_validation(args, want):
     assert brisk.lib().brisk_verify_commit(*args, None) == want
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(hv=None), ENULL), (dict(acc=None), ENULL), (dict(lm=None), ENULL), (dict(B=0), ESHAPE),
+    (dict(K=0), ESHAPE), (dict(K=65), ESHAPE), (dict(d=4100), EUNSUP), (dict(hv=MISALIGNED), EUNSUP),
+    (dict(ce=MISALIGNED), EUNSUP),
+])
+def test_corrector_loss_validation(kw, want):
+    a = dict(hv=FAKE, W=FAKE, ids=FAKE, cl=FAKE, ref=FAKE, acc=FAKE, B=2, L=8, K=8, d=4096, V=126464,
+             beta=0.01, lp=FAKE, ce=None, kl=None, mean=FAKE, lm=FAKE)
+    a.update(kw)
+    st = brisk.lib().brisk_corrector_loss(a["hv"], a["lm"], a["ids"], a["cl"], a["ref"], a["acc"], a["B"],
+                                          a["L"], a["K"], a["d"], a["V"], a["beta"], a["lp"], a["ce"],
+                                          a["kl"], a["mean"], None)
+    assert st == want

@@ -1,0 +1,52 @@
+"""GPU parity of the corrector's training loss (brisk_corrector_loss) against
+the CPU oracle, on the decoding path's own candidates, refined logits and
+accept lengths."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import synth
+
+pytestmark = pytest.mark.gpu
+
+brisk = pytest.importorskip("paper_2609_33390_amd")
+
+
+def _run(wl, psi_std=0.02, sigma=0.3):
+    blk = synth.make_block(wl, "cuda", psi_std=psi_std)
+    cl, ci = brisk.propose_block(blk.H, blk.W, wl.K)
+    corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
+    rr = brisk.rerank(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, wl.B, wl.L, want_scores=True)
+    acc, _ = brisk.verify_accept(rr["selected"], blk.verifier)
+    g = torch.Generator(device="cuda").manual_seed(3)
+    Hv = (blk.H.float() + sigma * torch.randn(blk.H.shape, generator=g, device="cuda")).to(torch.bfloat16)
+    out = brisk.corrector_loss(Hv, blk.W, ci, cl, rr["refined"], acc, wl.B, wl.L)
+    torch.cuda.synchronize()
+    g_out = {k: v.cpu().numpy() for k, v in out.items()}
+    o = oracle.corrector_loss(oracle.bf16_to_f64(synth.bf16_bits(Hv)), synth.bf16_bits(blk.W),
+                              ci.cpu().numpy(), cl.cpu().numpy().astype(np.float64),
+                              rr["refined"].cpu().numpy().astype(np.float64), acc.cpu().numpy(), wl.L)
+    return g_out, o
+
+
+def _check(g, o):
+    assert np.all(g["loss_pos"][~o["mask"]] == 0.0)   # unreached positions contribute nothing
+    np.testing.assert_allclose(g["loss_pos"], o["loss_pos"], rtol=1e-3, atol=2e-3)
+    np.testing.assert_allclose(g["ce"][o["mask"]], o["ce"][o["mask"]], rtol=1e-3, atol=2e-3)
+    np.testing.assert_allclose(g["kl"][o["mask"]], o["kl"][o["mask"]], rtol=1e-3, atol=2e-3)
+    assert int(g["loss_mean"][1]) == o["count"]
+    assert g["loss_mean"][0] == pytest.approx(o["mean"], rel=1e-3, abs=1e-3)
+
+
+@pytest.mark.parametrize("name", ["tiny-d64-v512", "llada8b-b1-l32"])
+def test_loss_matches_oracle(name):
+    _check(*_run(synth.WORKLOADS[name]))
+
+
+@pytest.mark.parametrize("B,L,K,d,V", [(5, 7, 16, 136, 900), (33, 4, 5, 64, 300), (2, 40, 64, 72, 700)])
+def test_loss_ragged_and_scaled_corrector(B, L, K, d, V):
+    wl = synth.Workload("lossr", B=B, L=L, d=d, V=V, K=K, r=32, sigma=0.3, flat_frac=0.5, seed=B + L + K)
+    g, o = _run(wl, psi_std=0.2)
+    _check(g, o)
+    assert 0 < o["count"] <= B * L

@@ -358,3 +358,58 @@ def test_verifier_argmax_ties_and_planted_row():
     assert list(oracle.verifier_argmax(bits(H), bits(W))) == [2, 2]
     H[1, 0] = -1.0           # now row 5 (-3 * -1 = 3) is the largest
     assert list(oracle.verifier_argmax(bits(H), bits(W))) == [2, 5]
+
+
+def _softmax(x):
+    e = np.exp(x - np.max(x))
+    return e / e.sum()
+
+
+def _loss_case(seed, K=5, B=2, L=3, d=8, V=11):
+    rng = np.random.default_rng(seed)
+    H = rng.standard_normal((B * L, d))
+    W = rng.standard_normal((V, d)).astype(np.float32)
+    W_bits = (W.view(np.uint32) >> 16).astype(np.uint16)
+    ids = np.stack([rng.choice(V, K, replace=False) for _ in range(B * L)]).astype(np.int32)
+    cl = rng.standard_normal((B * L, K))
+    ref = rng.standard_normal((B * L, K))
+    return H, W_bits, ids, cl, ref
+
+
+def test_corrector_loss_hand_formula():
+    H, W_bits, ids, cl, ref = _loss_case(0)
+    acc = np.array([3, 0])
+    out = oracle.corrector_loss(H, W_bits, ids, cl, ref, acc, 3, beta=0.25)
+    W = oracle.bf16_to_f64(W_bits)
+    for r in range(6):
+        lp = np.array([W[v] @ H[r] for v in ids[r]])
+        p, q, rr = _softmax(lp), _softmax(cl[r]), _softmax(ref[r])
+        want = -np.sum(p * np.log(rr)) + 0.25 * np.sum(q * np.log(q / rr))
+        assert out["ce"][r] + 0.25 * out["kl"][r] == pytest.approx(want, rel=1e-12)
+    # block 0 fully accepted: all 3 positions; block 1 rejected at position 1: only it
+    assert list(out["mask"]) == [True, True, True, True, False, False]
+    assert out["count"] == 4
+    assert out["mean"] == pytest.approx(out["loss_pos"].sum() / 4, rel=1e-15)
+
+
+def test_corrector_loss_special_cases():
+    H, W_bits, ids, cl, ref = _loss_case(1)
+    acc = np.array([3, 3])
+    # refined equal to the base logits: the KL term vanishes
+    out = oracle.corrector_loss(H, W_bits, ids, cl, cl, acc, 3)
+    assert np.allclose(out["kl"], 0.0, atol=1e-14)
+    # refined logits that reproduce the verifier distribution: CE = its entropy (the minimum)
+    W = oracle.bf16_to_f64(W_bits)
+    lp = np.stack([[W[v] @ H[r] for v in ids[r]] for r in range(6)])
+    out2 = oracle.corrector_loss(H, W_bits, ids, cl, lp + 3.0, acc, 3)
+    ent = np.array([-np.sum(_softmax(x) * np.log(_softmax(x))) for x in lp])
+    assert np.allclose(out2["ce"], ent, rtol=1e-12)
+    out3 = oracle.corrector_loss(H, W_bits, ids, cl, ref, acc, 3)
+    assert np.all(out3["ce"] >= ent - 1e-12) and np.all(out3["kl"] >= -1e-14)
+
+
+def test_reached_mask_brute_force():
+    for L in (1, 4, 7):
+        for a in range(L + 1):
+            m = oracle.reached_mask(np.array([a]), L)[0]
+            assert list(m) == [j <= a for j in range(L)]
