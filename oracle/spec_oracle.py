@@ -21,8 +21,9 @@ from its published definition: ten rounds of two 32x32->64-bit products with
 the multipliers 0xD2511F53 and 0xCD9E8D57 and a Weyl key schedule with
 increments 0x9E3779B9 and 0xBB67AE85.  Token v of row i uses output word
 v mod 4 of the block counter (v div 4, i, 0, 0) under the key (seed low
-word, seed high word); the word u maps to U = (floor(u / 256) + 1/2) / 2^24
-in (0, 1) and G = -log(-log U).
+word, seed high word); the word u maps to U = (floor(u / 512) + 1/2) / 2^23,
+a value strictly inside (0, 1) that single precision holds exactly, and
+G = -log(-log U).
 
 Readings (also in the design notes): R21 p_i is the verifier softmax at
 temperature T over the whole vocabulary; R22 pi_i is given as probabilities
@@ -73,7 +74,7 @@ def gumbel_for(rows: np.ndarray, V: int, seed: int) -> np.ndarray:
     ctr[..., 0] = np.arange(nb, dtype=np.uint32)[None, :]
     ctr[..., 1] = rows[:, None]
     words = philox4x32_10(ctr, (seed & 0xFFFFFFFF, seed >> 32)).reshape(len(rows), nb * 4)[:, :V]
-    U = ((words >> np.uint32(8)).astype(np.float64) + 0.5) / float(1 << 24)
+    U = ((words >> np.uint32(9)).astype(np.float64) + 0.5) / float(1 << 23)
     return -np.log(-np.log(U))
 
 
