@@ -163,6 +163,37 @@ def time_corrector_loss(brisk, blk, wl, corr, cl, ci, acc, reps=50):
     return {"positions": wl.B * wl.L, "us_per_call": round(e0.elapsed_time(e1) * 1e3 / reps, 2)}
 
 
+def time_spec_verify(brisk, blk, wl, cl, ci, reps=20):
+    """brisk_spec_verify on verifier rows bf16(hidden + 0.3 noise), proposals
+    drawn from the softmax of the candidate logits mixed with the uniform law
+    (weight 0.3), temperature 1, fresh seed per call."""
+    import torch
+
+    g = torch.Generator(device=blk.H.device).manual_seed(3)
+    Hv = (blk.H.float() + 0.3 * torch.randn(blk.H.shape, generator=g, device=blk.H.device)).to(torch.bfloat16)
+    prob = (0.7 * torch.softmax(cl.float(), dim=1) + 0.3 / wl.K).contiguous()
+    pick = torch.multinomial(prob, 1, generator=g).view(-1)
+    x = ci.gather(1, pick[:, None]).view(wl.B, wl.L).contiguous()
+    u = torch.rand(wl.B * wl.L, generator=g, device=blk.H.device)
+    calls = [0]
+
+    def fn():
+        calls[0] += 1
+        return brisk.spec_verify(Hv, blk.W, x, ci, prob, u, 1000 + calls[0], 1.0)
+
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        out = fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return {"positions": wl.B * wl.L, "us_per_call": round(e0.elapsed_time(e1) * 1e3 / reps, 2),
+            "mean_accept_len": round(out["accept_len"].float().mean().item(), 3)}
+
+
 def copy_calibration(n_bytes=1 << 30, reps=3):
     """A plain streaming kernel of known size (read n_bytes, write n_bytes),
     run so that HBM byte counters can be scaled against it."""
@@ -319,6 +350,7 @@ def main():
     prof = time_accept_profile(brisk, dev, wl.L)
     fused = time_fused_verify(brisk, blk, wl)
     loss = time_corrector_loss(brisk, blk, wl, corr, cl, ci, acc)
+    spec = time_spec_verify(brisk, blk, wl, cl, ci)
     res = {
         "metric": METRIC, "value": round(value, 1), "unit": "block positions/s", "n_gpus": 1,
         "steps": n, "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
@@ -333,6 +365,7 @@ def main():
         "accept_profile": prof,
         "propose_verify": fused,
         "corrector_loss": loss,
+        "spec_verify": spec,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(blk, args.cpu_budget_s)

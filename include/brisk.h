@@ -211,6 +211,44 @@ int brisk_verify_commit(const int32_t* proposal, const int32_t* verifier, int32_
                         int32_t* accept_len, int32_t* committed, int32_t* n_committed,
                         void* stream);
 
+/* Workspace bytes brisk_spec_verify needs (written to *bytes). */
+int brisk_spec_verify_workspace_size(int32_t B, int32_t L, int32_t V, int32_t K, size_t* bytes);
+
+/*
+ * Stochastic speculative verification (Section 3.3; Algorithm 1(b) verify
+ * and commit).  Position i of block b (row r = b * L + i) accepts its
+ * proposal x_r with probability min{1, p_r(x_r) / pi_r(x_r)}, where p_r is
+ * the verifier's softmax at temperature T over the whole vocabulary (logits
+ * <lm_head[v], ver_hidden[r]>, one fused LM-head pass with an online
+ * log-sum-exp) and pi_r the proposal law over the position's candidates.
+ * Each row also draws y_r from the normalised positive part [p_r - pi_r]_+,
+ * which keeps the committed token distributed as p_r; the block stops at its
+ * first rejection a and commits y at position a.
+ *
+ *   ver_hidden  [B*L, d] bf16    verifier hidden states
+ *   lm_head     [V, d]   bf16
+ *   proposal    [B, L]   int32   x
+ *   cand_id     [B*L, K] int32   distinct candidate ids of each position
+ *   cand_prob   [B*L, K] fp32    pi over those ids (tokens outside have pi = 0)
+ *   u_accept    [B*L]    fp32    uniforms in [0, 1) for the accept tests
+ *   seed        key of the Philox4x32-10 generator of the residual draws
+ *               (Gumbel variate of token v at row r from word v mod 4 of
+ *               counter (v / 4, r, 0, 0))
+ *   accept_len  [B] int32 out;  correction [B] int32 out, nullable (-1 when
+ *               the block is fully accepted)
+ *   row_accept, row_resample  [B*L] int32 out, nullable: every position's
+ *               accept decision (1/0) and residual draw
+ *   ws          device scratch of brisk_spec_verify_workspace_size bytes
+ *
+ * Limits: 1 <= K <= 64, K < V, temperature > 0, B*L <= 2^20, and the LM-head
+ * limits of brisk_propose_block.
+ */
+int brisk_spec_verify(const uint16_t* ver_hidden, const uint16_t* lm_head, const int32_t* proposal,
+                      const int32_t* cand_id, const float* cand_prob, const float* u_accept,
+                      uint64_t seed, float temperature, int32_t B, int32_t L, int32_t K, int32_t d,
+                      int32_t V, int32_t* accept_len, int32_t* correction, int32_t* row_accept,
+                      int32_t* row_resample, void* ws, size_t ws_bytes, void* stream);
+
 /*
  * Corrector training loss, forward (Appendix "Candidate-Refinement Head
  * Details", Eq. head_training_loss).  For position j of block b (row

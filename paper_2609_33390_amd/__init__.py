@@ -15,6 +15,7 @@ Entry points (same names as the C ABI):
   verifier rows (argmax);
 * :func:`verify_commit` - greedy verification and the committed tokens;
 * :func:`corrector_loss` - the corrector's training loss on reached positions;
+* :func:`spec_verify` - stochastic speculative verification with residual draws;
 * :func:`accept_profile` - acceptance profile, tokens per forward and the
   risk-reward position weights from many blocks' accept lengths.
 """
@@ -28,14 +29,15 @@ from typing import Dict, Optional, Tuple
 import torch
 
 __all__ = ["BriskError", "Corrector", "propose_block", "rerank", "verify_accept", "accept_profile",
-           "propose_verify", "verify_commit", "corrector_loss",
+           "propose_verify", "verify_commit", "corrector_loss", "spec_verify",
            "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
 ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
                "brisk_propose_block", "brisk_rerank_workspace_size", "brisk_rerank",
                "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
-               "brisk_verify_commit", "brisk_corrector_loss", "brisk_accept_profile_workspace_size",
+               "brisk_verify_commit", "brisk_spec_verify_workspace_size", "brisk_spec_verify",
+               "brisk_corrector_loss", "brisk_accept_profile_workspace_size",
                "brisk_accept_profile")
 PSI_FIELDS = ("A_h", "A_e", "P_h", "P_e", "pos_emb", "P_phi", "W_z", "W_h", "W_s", "W_c", "w_g")
 
@@ -95,6 +97,11 @@ def lib() -> ctypes.CDLL:
                                                _sz, _p]
             L.brisk_verify_commit.restype = ctypes.c_int
             L.brisk_verify_commit.argtypes = [_p, _p, _i32, _i32, _p, _p, _p, _p]
+            L.brisk_spec_verify_workspace_size.restype = ctypes.c_int
+            L.brisk_spec_verify_workspace_size.argtypes = [_i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
+            L.brisk_spec_verify.restype = ctypes.c_int
+            L.brisk_spec_verify.argtypes = [_p, _p, _p, _p, _p, _p, ctypes.c_uint64, ctypes.c_float,
+                                            _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _sz, _p]
             L.brisk_corrector_loss.restype = ctypes.c_int
             L.brisk_corrector_loss.argtypes = [_p, _p, _p, _p, _p, _p, _i32, _i32, _i32, _i32, _i32,
                                                ctypes.c_float, _p, _p, _p, _p, _p]
@@ -384,4 +391,37 @@ def corrector_loss(ver_hidden: torch.Tensor, lm_head: torch.Tensor, cand_id: tor
                                     _ptr(out["loss_pos"]), _ptr(out["ce"]), _ptr(out["kl"]),
                                     _ptr(out["loss_mean"]), _stream_ptr(dev, stream))
     _check(st, "brisk_corrector_loss")
+    return out
+
+
+def spec_verify(ver_hidden: torch.Tensor, lm_head: torch.Tensor, proposal: torch.Tensor,
+                cand_id: torch.Tensor, cand_prob: torch.Tensor, u_accept: torch.Tensor, seed: int,
+                temperature: float = 1.0, *, workspace: Optional[torch.Tensor] = None,
+                stream=None) -> Dict[str, torch.Tensor]:
+    """Stochastic verification: ``accept_len``, ``correction`` [B] and the
+    per-position ``row_accept``, ``row_resample`` [B*L]."""
+    _dev_tensor(ver_hidden, "ver_hidden", torch.bfloat16, 2)
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
+    _dev_tensor(proposal, "proposal", torch.int32, 2)
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
+    _dev_tensor(cand_prob, "cand_prob", torch.float32, 2)
+    _dev_tensor(u_accept, "u_accept", torch.float32, 1)
+    B, L = proposal.shape
+    K = cand_id.shape[1]
+    d, V = ver_hidden.shape[1], lm_head.shape[0]
+    dev = ver_hidden.device
+    nbytes = _sz(0)
+    _check(lib().brisk_spec_verify_workspace_size(B, L, V, K, ctypes.byref(nbytes)),
+           "brisk_spec_verify_workspace_size")
+    ws = workspace if workspace is not None else _workspace(dev, nbytes.value, "spec")
+    out = {"accept_len": torch.empty(B, dtype=torch.int32, device=dev),
+           "correction": torch.empty(B, dtype=torch.int32, device=dev),
+           "row_accept": torch.empty(B * L, dtype=torch.int32, device=dev),
+           "row_resample": torch.empty(B * L, dtype=torch.int32, device=dev)}
+    st = lib().brisk_spec_verify(_ptr(ver_hidden), _ptr(lm_head), _ptr(proposal), _ptr(cand_id),
+                                 _ptr(cand_prob), _ptr(u_accept), int(seed) & ((1 << 64) - 1),
+                                 float(temperature), B, L, K, d, V, _ptr(out["accept_len"]),
+                                 _ptr(out["correction"]), _ptr(out["row_accept"]),
+                                 _ptr(out["row_resample"]), _ptr(ws), ws.numel(), _stream_ptr(dev, stream))
+    _check(st, "brisk_spec_verify")
     return out

@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 4;
+constexpr int kAbiVersion = 5;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 
@@ -203,6 +203,37 @@ int brisk_verify_commit(const int32_t* proposal, const int32_t* verifier, int32_
     return BRISK_ERR_UNSUPPORTED;
   brisk::launch_commit(proposal, verifier, B, L, accept_len, committed, n_committed,
                        static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_spec_verify_workspace_size(int32_t B, int32_t L, int32_t V, int32_t K, size_t* bytes) {
+  if (!bytes) return BRISK_ERR_NULL;
+  if (B < 1 || L < 1 || static_cast<int64_t>(B) * L > kMaxRows || K < 1 || K > 64 || V <= K)
+    return BRISK_ERR_SHAPE;
+  *bytes = brisk::spec_verify_workspace_bytes(B, L, V, K);
+  return BRISK_OK;
+}
+
+int brisk_spec_verify(const uint16_t* ver_hidden, const uint16_t* lm_head, const int32_t* proposal,
+                      const int32_t* cand_id, const float* cand_prob, const float* u_accept,
+                      uint64_t seed, float temperature, int32_t B, int32_t L, int32_t K, int32_t d,
+                      int32_t V, int32_t* accept_len, int32_t* correction, int32_t* row_accept,
+                      int32_t* row_resample, void* ws, size_t ws_bytes, void* stream) {
+  if (!proposal || !cand_id || !cand_prob || !u_accept || !accept_len) return BRISK_ERR_NULL;
+  if (B < 1 || L < 1 || static_cast<int64_t>(B) * L > kMaxRows || K < 1 || K > 64 || V <= K ||
+      !(temperature > 0.f) || temperature > 3.0e38f)
+    return BRISK_ERR_SHAPE;
+  const int st = lmhead_check(ver_hidden, lm_head, B * L, d, V, 1);
+  if (st != BRISK_OK) return st;
+  if (!aligned4(proposal) || !aligned4(cand_id) || !aligned4(cand_prob) || !aligned4(u_accept) ||
+      !aligned4(accept_len) || !aligned4(correction) || !aligned4(row_accept) || !aligned4(row_resample))
+    return BRISK_ERR_UNSUPPORTED;
+  const size_t need = brisk::spec_verify_workspace_bytes(B, L, V, K);
+  if (ws_bytes < need || !ws) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_spec_verify(ver_hidden, lm_head, B, L, d, V, K, proposal, cand_id, cand_prob, u_accept,
+                            seed, temperature, accept_len, correction, row_accept, row_resample, ws,
+                            static_cast<hipStream_t>(stream));
   return launch_status();
 }
 

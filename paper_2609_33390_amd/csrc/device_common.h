@@ -124,6 +124,38 @@ __device__ __forceinline__ float wave_allmax(float v) {
 
 __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + __expf(-x)); }
 
+// ---------------------------------------------------------------------------
+// Philox4x32-10 (Salmon, Moraes, Dror and Shaw, SC'11): ten rounds of two
+// 32x32 -> 64-bit products (multipliers 0xD2511F53, 0xCD9E8D57) and a Weyl
+// key schedule (increments 0x9E3779B9, 0xBB67AE85).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c;
+}
+
+// Gumbel variate of a generator word: U = (w / 512 + 1/2) / 2^23 lies
+// strictly inside (0, 1) and is exact in single precision; G = -log(-log U).
+__device__ __forceinline__ float gumbel_of(uint32_t w) {
+  const float U = (static_cast<float>(w >> 9) + 0.5f) * (1.0f / 8388608.0f);
+  return -__logf(-__logf(U));
+}
+
+// Merge a log-sum-exp partial (max m, sum of exp(x - m)) into (m, s).
+__device__ __forceinline__ void lse_combine(float& m, float& s, float2 o) {
+  const float M = fmaxf(m, o.x);
+  if (M == -INFINITY) return;
+  s = s * __expf(m - M) + o.y * __expf(o.x - M);
+  m = M;
+}
+
 __device__ __forceinline__ int clamp_id(int32_t id, int32_t V) {
   return id < 0 ? 0 : (id >= V ? V - 1 : id);
 }

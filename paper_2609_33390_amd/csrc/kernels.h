@@ -17,6 +17,14 @@ void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V
                     int rows_prop, float* cand_logit, int32_t* cand_id, int32_t* ver_token,
                     void* ws, hipStream_t s);
 
+// ---- stochastic speculative verification ------------------------------------
+size_t spec_verify_workspace_bytes(int B, int L, int V, int K);
+void launch_spec_verify(const uint16_t* Hv, const uint16_t* W, int B, int L, int d, int V, int K,
+                        const int32_t* proposal, const int32_t* cand_id, const float* cand_prob,
+                        const float* u_accept, uint64_t seed, float temperature, int32_t* accept_len,
+                        int32_t* correction, int32_t* row_accept, int32_t* row_resample, void* ws,
+                        hipStream_t s);
+
 // ---- rerank: hoisted projections + sequential scan -------------------------
 size_t rerank_workspace_bytes(const brisk_corrector& c, int B, int L, int K);
 void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint16_t* ctx_hidden,

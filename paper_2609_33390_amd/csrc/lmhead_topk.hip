@@ -94,14 +94,59 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
 // Whether the per-position lists fit in LDS for the in-workgroup merge (the
 // stage buffers are idle by then).
 template <class C, int KP>
-constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 <= C::LDS_BYTES;
+constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 + C::NT * 8 <= C::LDS_BYTES;
+
+// Verifier rows of stochastic verification: logits are scaled by 1/T, each
+// thread also keeps a running log-sum-exp (max, scaled sum) of its logits,
+// and the keys rank s + G (a Gumbel variate per token from Philox4x32-10
+// keyed by (key0, key1), counter (token / 4, row, 0, 0), word token % 4).
+struct SampleArgs {
+  float inv_T;
+  uint32_t key0, key1;
+  float2* lse_part;         // [rows, n_parts] (max, sum of exp(s - max))
+  const int32_t* cand_id;   // [rows, K]: tokens kept out of the key lists
+  int K;
+};
+
+// Candidate filter of a row: bit (id mod 64) of a 64-bit mask is set for
+// every candidate id (clamped into [0, V) as everywhere else), so a clear bit
+// rules a token out at once; a set bit is settled against the ids themselves,
+// loaded eight at a time so one memory latency covers eight of them.
+__device__ __forceinline__ uint64_t candidate_mask(const SampleArgs& sa, int r, int V) {
+  const int32_t* ids = sa.cand_id + static_cast<size_t>(r) * sa.K;
+  uint64_t m = 0;
+  for (int k0 = 0; k0 < sa.K; k0 += 8) {
+    int32_t t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t[q] = k0 + q < sa.K ? ids[k0 + q] : -1;
+#pragma unroll
+    for (int q = 0; q < 8; ++q)
+      if (k0 + q < sa.K) m |= 1ull << (clamp_id(t[q], V) & 63);
+  }
+  return m;
+}
+
+__device__ __forceinline__ bool is_candidate(const SampleArgs& sa, uint64_t mask, int r, int v, int V) {
+  if (!((mask >> (v & 63)) & 1ull)) return false;
+  const int32_t* ids = sa.cand_id + static_cast<size_t>(r) * sa.K;
+  int hit = 0;
+  for (int k0 = 0; k0 < sa.K; k0 += 8) {
+    int32_t t[8];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) t[q] = k0 + q < sa.K ? ids[k0 + q] : -1;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) hit |= (k0 + q < sa.K) & (clamp_id(t[q], V) == v);
+  }
+  return hit != 0;
+}
 
 // One workgroup per compute unit (the LDS footprint allows no more), so the
 // compiler may split the whole register file among the workgroup's waves.
-template <class C, int KP>
+template <class C, int KP, bool SAMPLE = false>
 __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4, C::NW / 4))) void lmhead_topk_kernel(
     const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int rows, int d, int V,
-    int n_rtiles, int n_vtiles, int tiles_per_group, uint64_t* __restrict__ partial, int n_parts) {
+    int n_rtiles, int n_vtiles, int tiles_per_group, uint64_t* __restrict__ partial, int n_parts,
+    SampleArgs sa) {
   __shared__ __align__(16) unsigned char smem[C::LDS_BYTES];
 
   const int tid = threadIdx.x, lane = tid & 63;
@@ -166,6 +211,19 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
   float thr = -INFINITY;  // logits below this cannot enter the list
+  float lse_m = -INFINITY, lse_s = 0.f;  // SAMPLE: running log-sum-exp
+  // The sampling epilogue keeps at most two generator blocks live (one in
+  // the large-row tile), and so does a 64-key list: unrolled further, the
+  // large-row tile runs out of registers and the others outgrow the full
+  // unroll of the chunk loop, whose accumulator indexing must stay static.
+  constexpr int kColFull = C::EPI_V / (C::TPP * 4);
+  constexpr int kColTwo = kColFull < 2 ? kColFull : 2;
+  constexpr int kColUnroll = SAMPLE ? (C::BR >= 128 ? 1 : kColTwo) : (KP >= 64 ? kColTwo : kColFull);
+  const bool row_ok = r0 + ep < rows;
+  uint64_t cmask = 0;
+  if constexpr (SAMPLE) {
+    if (row_ok) cmask = candidate_mask(sa, r0 + ep, V);
+  }
 
   floatx4 acc[C::TV][C::TR];
 #pragma unroll
@@ -234,9 +292,30 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
       }
       lds_sync();
-#pragma unroll
+#pragma unroll kColUnroll
       for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) {
-        const floatx4 v = *reinterpret_cast<const floatx4*>(sE + ep * C::EPI_V + epi_slot(ep, col >> 2) * 4);
+        floatx4 v = *reinterpret_cast<const floatx4*>(sE + ep * C::EPI_V + epi_slot(ep, col >> 2) * 4);
+        if constexpr (SAMPLE) {
+          const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);  // a multiple of 4
+          float m4 = -INFINITY;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            v[q] *= sa.inv_T;
+            if (vid0 + q < V) m4 = fmaxf(m4, v[q]);
+          }
+          if (m4 > lse_m) {
+            lse_s *= __expf(lse_m - m4);
+            lse_m = m4;
+          }
+          const uint4 w = philox4x32_10(make_uint4(static_cast<uint32_t>(vid0) >> 2, static_cast<uint32_t>(r0 + ep), 0u, 0u),
+                                        sa.key0, sa.key1);
+          const uint32_t wq[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (vid0 + q < V) lse_s += __expf(v[q] - lse_m);
+            v[q] += gumbel_of(wq[q]);
+          }
+        }
         // common case: none of the four logits reaches the list's smallest
         // entry, which one float compare decides; only then build keys
         const float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
@@ -246,7 +325,13 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
           for (int q = 0; q < 4; ++q) {
             const int vid = vid0 + q;
             const uint64_t key = make_key(v[q], static_cast<uint32_t>(vid));
-            if (vid < V && key > list[KP - 1]) list_insert(list, key);
+            if (vid < V && key > list[KP - 1]) {
+              // sampling keeps candidates out: their draws use exact weights
+              if constexpr (SAMPLE) {
+                if (!row_ok || is_candidate(sa, cmask, r0 + ep, vid, V)) continue;
+              }
+              list_insert(list, key);
+            }
           }
           thr = list_floor(list[KP - 1]);
         }
@@ -261,8 +346,10 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   const int r = r0 + ep;
   if constexpr (kWgMerge<C, KP>) {
     uint64_t* sk = reinterpret_cast<uint64_t*>(smem);
+    float2* sl = reinterpret_cast<float2*>(smem + C::NT * KP * 8);
 #pragma unroll
     for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
+    if constexpr (SAMPLE) sl[tid] = make_float2(lse_m, lse_s);
     lds_sync();
 #pragma unroll
     for (int s = C::TPP / 2; s >= 1; s >>= 1) {
@@ -275,6 +362,10 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         }
 #pragma unroll
         for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
+        if constexpr (SAMPLE) {
+          lse_combine(lse_m, lse_s, sl[other]);
+          sl[tid] = make_float2(lse_m, lse_s);
+        }
       }
       lds_sync();
     }
@@ -282,13 +373,15 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       uint64_t* dst = partial + (static_cast<size_t>(r) * n_parts + group) * KP;
 #pragma unroll
       for (int j = 0; j < KP; ++j) dst[j] = list[j];
+      if constexpr (SAMPLE) sa.lse_part[static_cast<size_t>(r) * n_parts + group] = make_float2(lse_m, lse_s);
     }
   } else {
     if (r < rows) {
-      uint64_t* dst =
-          partial + (static_cast<size_t>(r) * n_parts + static_cast<size_t>(group) * C::TPP + esub) * KP;
+      const size_t part = static_cast<size_t>(r) * n_parts + static_cast<size_t>(group) * C::TPP + esub;
+      uint64_t* dst = partial + part * KP;
 #pragma unroll
       for (int j = 0; j < KP; ++j) dst[j] = list[j];
+      if constexpr (SAMPLE) sa.lse_part[part] = make_float2(lse_m, lse_s);
     }
   }
 }
@@ -422,12 +515,160 @@ Plan make_plan(int rows, int V, int K) {
   return make_plan_for<LargeRows>(2, rows, V, K);
 }
 
-template <class C, int KP>
+template <class C, int KP, bool SAMPLE = false>
 void launch_tile(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, int d, int V,
-                 uint64_t* partial, hipStream_t s) {
+                 uint64_t* partial, hipStream_t s, SampleArgs sa = SampleArgs{}) {
   const int nblocks = p.n_rtiles * p.n_groups;
-  hipLaunchKernelGGL((lmhead_topk_kernel<C, KP>), dim3(nblocks), dim3(C::NT), 0, s, H, W, rows, d,
-                     V, p.n_rtiles, p.n_vtiles, p.tiles_per_group, partial, p.n_parts);
+  hipLaunchKernelGGL((lmhead_topk_kernel<C, KP, SAMPLE>), dim3(nblocks), dim3(C::NT), 0, s, H, W, rows,
+                     d, V, p.n_rtiles, p.n_vtiles, p.tiles_per_group, partial, p.n_parts, sa);
+}
+
+// ---------------------------------------------------------------------------
+// Stochastic speculative verification (Section 3.3): per verifier row r, the
+// accept test of the proposal x_r against min{1, p_r(x_r) / pi_r(x_r)} and a
+// draw y_r from [p_r - pi_r]_+ by Gumbel-max.  Only the K candidates carry
+// proposal mass, so every other token competes with score s + G - lse
+// (s = logit / T): the LM-head pass leaves, per (row, group), the largest
+// keys of s + G over the non-candidate tokens and a log-sum-exp partial.  One
+// workgroup per row: merge keys and partials, take the verifier logits of the
+// candidates and of x_r by dot products, then decide.
+// ---------------------------------------------------------------------------
+template <int KP>
+__global__ __launch_bounds__(256) void spec_row_kernel(
+    const uint64_t* __restrict__ partial, const float2* __restrict__ lse_part, int n_parts,
+    const uint16_t* __restrict__ Hv, const uint16_t* __restrict__ W, int d, int V, int K,
+    const int32_t* __restrict__ proposal, const int32_t* __restrict__ cand_id,
+    const float* __restrict__ cand_prob, const float* __restrict__ u_accept, float inv_T,
+    uint32_t key0, uint32_t key1, int32_t* __restrict__ row_accept, int32_t* __restrict__ row_resample) {
+  constexpr int NT = 256, NW = NT / kWave, BATCH = 8;
+  __shared__ uint64_t sk[NW][KP];
+  __shared__ float2 s_lse[NT];
+  __shared__ float s_logit[kWave + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row = blockIdx.x;
+
+  // (1) keys of s + G: per-lane lists, wave butterflies, then across waves
+  const int n_keys = n_parts * KP;
+  const uint64_t* src = partial + static_cast<size_t>(row) * n_keys;
+  uint64_t list[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) list[j] = 0;
+  for (int i0 = tid; i0 < n_keys; i0 += NT * BATCH) {
+    uint64_t kb[BATCH];
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q) {
+      const int i = i0 + q * NT;
+      kb[q] = i < n_keys ? src[i] : 0ull;
+    }
+#pragma unroll
+    for (int q = 0; q < BATCH; ++q)
+      if (kb[q] > list[KP - 1]) list_insert(list, kb[q]);
+  }
+#pragma unroll
+  for (int m = 1; m < kWave; m <<= 1) butterfly_merge(list, m);
+  if (lane == 0) {
+#pragma unroll
+    for (int j = 0; j < KP; ++j) sk[wave][j] = list[j];
+  }
+  // (2) log-sum-exp partials, combined in a fixed order
+  float m = -INFINITY, sm = 0.f;
+  for (int i = tid; i < n_parts; i += NT) lse_combine(m, sm, lse_part[static_cast<size_t>(row) * n_parts + i]);
+  s_lse[tid] = make_float2(m, sm);
+  // (3) verifier logits of the candidates (k < K) and of the proposal (k = K)
+  const uint16_t* h = Hv + static_cast<size_t>(row) * d;
+  const int x = clamp_id(proposal[row], V);
+  for (int k = wave; k <= K; k += NW) {
+    const int v = k < K ? clamp_id(cand_id[static_cast<size_t>(row) * K + k], V) : x;
+    const uint16_t* w = W + static_cast<size_t>(v) * d;
+    float acc = 0.f;
+    for (int c = lane * 8; c < d; c += kWave * 8) {
+      const uint4 a = *reinterpret_cast<const uint4*>(w + c);
+      const uint4 b = *reinterpret_cast<const uint4*>(h + c);
+      acc += bf16_lo(a.x) * bf16_lo(b.x) + bf16_hi(a.x) * bf16_hi(b.x);
+      acc += bf16_lo(a.y) * bf16_lo(b.y) + bf16_hi(a.y) * bf16_hi(b.y);
+      acc += bf16_lo(a.z) * bf16_lo(b.z) + bf16_hi(a.z) * bf16_hi(b.z);
+      acc += bf16_lo(a.w) * bf16_lo(b.w) + bf16_hi(a.w) * bf16_hi(b.w);
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) s_logit[k] = acc;
+  }
+  __syncthreads();
+  for (int st = NT / 2; st >= 1; st >>= 1) {
+    if (tid < st) {
+      float2 me = s_lse[tid];
+      lse_combine(me.x, me.y, s_lse[tid + st]);
+      s_lse[tid] = me;
+    }
+    __syncthreads();
+  }
+  if (wave != 0) return;
+#pragma unroll
+  for (int j = 0; j < KP; ++j) list[j] = lane < NW ? sk[lane][j] : 0ull;
+#pragma unroll
+  for (int mm = 1; mm < NW; mm <<= 1) butterfly_merge(list, mm);
+  if (lane != 0) return;
+
+  // (4) decisions, in lane 0, with the accurate exp / log: where p_r and
+  // pi_r nearly cancel, the residual weight needs every bit fp32 has
+  const float lse = s_lse[0].x + logf(s_lse[0].y);
+  const int32_t* ids = cand_id + static_cast<size_t>(row) * K;
+  const float* pis = cand_prob + static_cast<size_t>(row) * K;
+  float pi_x = 0.f;
+  for (int k = 0; k < K; ++k)
+    if (clamp_id(ids[k], V) == x) pi_x += pis[k];
+  const float p_x = expf(s_logit[K] * inv_T - lse);
+  const bool accept = pi_x <= 0.f || u_accept[row] < fminf(1.f, p_x / pi_x);
+  // residual draw: candidates from their exact weights, everyone else from
+  // the best key (no candidate enters the lists; score s + G - lse)
+  float best = -INFINITY;
+  int best_id = 0x7FFFFFFF;
+  for (int k = 0; k < K; ++k) {
+    const int v = clamp_id(ids[k], V);
+    const float w = expf(s_logit[k] * inv_T - lse) - pis[k];
+    if (w <= 0.f) continue;
+    const uint4 g4 = philox4x32_10(make_uint4(static_cast<uint32_t>(v) >> 2, static_cast<uint32_t>(row), 0u, 0u),
+                                   key0, key1);
+    const uint32_t gw[4] = {g4.x, g4.y, g4.z, g4.w};
+    const float sc = logf(w) + gumbel_of(gw[v & 3]);
+    if (sc > best || (sc == best && v < best_id)) {
+      best = sc;
+      best_id = v;
+    }
+  }
+  if (list[0] != 0) {
+    const int v = key_id(list[0]);
+    const float sc = key_logit(list[0]) - lse;
+    if (sc > best || (sc == best && v < best_id)) {
+      best = sc;
+      best_id = v;
+    }
+  }
+  row_accept[row] = accept ? 1 : 0;
+  row_resample[row] = best_id == 0x7FFFFFFF ? x : best_id;
+}
+
+// First rejected position of each block and the token drawn there.
+__global__ __launch_bounds__(256) void spec_commit_kernel(const int32_t* __restrict__ row_accept,
+                                                          const int32_t* __restrict__ row_resample,
+                                                          int B, int L, int32_t* __restrict__ accept_len,
+                                                          int32_t* __restrict__ correction) {
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (b >= B) return;
+  const size_t base = static_cast<size_t>(b) * L;
+  int a = L;
+  for (int c = 0; c < L; c += 64) {
+    const int i = c + lane;
+    const uint64_t mask = __ballot(i < L && row_accept[base + i] == 0);
+    if (mask) {
+      a = c + __builtin_ctzll(mask);
+      break;
+    }
+  }
+  if (lane == 0) {
+    accept_len[b] = a;
+    if (correction) correction[b] = a < L ? row_resample[base + a] : -1;
+  }
 }
 
 template <int KP>
@@ -443,7 +684,61 @@ void launch_kp(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, in
                      p.n_parts * KP, K, rows_prop, cand_logit, cand_id, ver_token);
 }
 
+template <int KP>
+void launch_spec_kp(const Plan& p, const uint16_t* Hv, const uint16_t* W, int B, int L, int d, int V, int K,
+                    const int32_t* proposal, const int32_t* cand_id, const float* cand_prob,
+                    const float* u_accept, SampleArgs sa, uint64_t* partial, int32_t* row_accept,
+                    int32_t* row_resample, int32_t* accept_len, int32_t* correction, hipStream_t s) {
+  const int rows = B * L;
+  switch (p.cfg) {
+    case 0: launch_tile<SmallRows, KP, true>(p, Hv, W, rows, d, V, partial, s, sa); break;
+    case 1: launch_tile<MidRows, KP, true>(p, Hv, W, rows, d, V, partial, s, sa); break;
+    default: launch_tile<LargeRows, KP, true>(p, Hv, W, rows, d, V, partial, s, sa); break;
+  }
+  hipLaunchKernelGGL((spec_row_kernel<KP>), dim3(rows), dim3(256), 0, s, partial, sa.lse_part, p.n_parts,
+                     Hv, W, d, V, K, proposal, cand_id, cand_prob, u_accept, sa.inv_T, sa.key0, sa.key1,
+                     row_accept, row_resample);
+  hipLaunchKernelGGL(spec_commit_kernel, dim3((B + 3) / 4), dim3(256), 0, s, row_accept, row_resample, B,
+                     L, accept_len, correction);
+}
+
+struct SpecLayout {
+  Plan plan;
+  size_t keys, lse, rows_acc, rows_res, total;
+};
+
+SpecLayout spec_layout(int B, int L, int V, int K) {
+  SpecLayout l{};
+  const int rows = B * L;
+  l.plan = make_plan(rows, V, 1);  // the best non-candidate key per row
+  auto up = [](size_t n) { return (n + 255) / 256 * 256; };
+  l.keys = 0;
+  l.lse = up(static_cast<size_t>(rows) * l.plan.n_parts * l.plan.KP * sizeof(uint64_t));
+  l.rows_acc = l.lse + up(static_cast<size_t>(rows) * l.plan.n_parts * sizeof(float2));
+  l.rows_res = l.rows_acc + up(static_cast<size_t>(rows) * sizeof(int32_t));
+  l.total = l.rows_res + up(static_cast<size_t>(rows) * sizeof(int32_t));
+  return l;
+}
+
 }  // namespace
+
+size_t spec_verify_workspace_bytes(int B, int L, int V, int K) { return spec_layout(B, L, V, K).total; }
+
+void launch_spec_verify(const uint16_t* Hv, const uint16_t* W, int B, int L, int d, int V, int K,
+                        const int32_t* proposal, const int32_t* cand_id, const float* cand_prob,
+                        const float* u_accept, uint64_t seed, float temperature, int32_t* accept_len,
+                        int32_t* correction, int32_t* row_accept, int32_t* row_resample, void* ws,
+                        hipStream_t s) {
+  const SpecLayout l = spec_layout(B, L, V, K);
+  char* base = static_cast<char*>(ws);
+  SampleArgs sa{1.0f / temperature, static_cast<uint32_t>(seed), static_cast<uint32_t>(seed >> 32),
+                reinterpret_cast<float2*>(base + l.lse), cand_id, K};
+  uint64_t* partial = reinterpret_cast<uint64_t*>(base + l.keys);
+  int32_t* ra = row_accept ? row_accept : reinterpret_cast<int32_t*>(base + l.rows_acc);
+  int32_t* rr = row_resample ? row_resample : reinterpret_cast<int32_t*>(base + l.rows_res);
+  launch_spec_kp<4>(l.plan, Hv, W, B, L, d, V, K, proposal, cand_id, cand_prob, u_accept, sa, partial, ra, rr,
+                    accept_len, correction, s);
+}
 
 size_t propose_workspace_bytes(int rows, int V, int K) {
   const Plan p = make_plan(rows, V, K);

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 4
+    assert L.brisk_abi_version() == 5
     for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5):
         assert L.brisk_status_str(st).decode()
     assert L.brisk_status_str(123).decode() == "unknown status"
@@ -199,4 +199,20 @@ def test_corrector_loss_validation(kw, want):
     st = brisk.lib().brisk_corrector_loss(a["hv"], a["lm"], a["ids"], a["cl"], a["ref"], a["acc"], a["B"],
                                           a["L"], a["K"], a["d"], a["V"], a["beta"], a["lp"], a["ce"],
                                           a["kl"], a["mean"], None)
+    assert st == want
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(prop=None), ENULL), (dict(u=None), ENULL), (dict(acc=None), ENULL), (dict(hv=None), ENULL),
+    (dict(K=0), ESHAPE), (dict(K=65), ESHAPE), (dict(T=0.0), ESHAPE), (dict(T=float("nan")), ESHAPE),
+    (dict(V=8, K=8), ESHAPE), (dict(d=4100), EUNSUP), (dict(cpr=MISALIGNED), EUNSUP),
+    (dict(ws_bytes=0), EWS),
+])
+def test_spec_verify_validation(kw, want):
+    a = dict(hv=FAKE, W=FAKE, prop=FAKE, cid=FAKE, cpr=FAKE, u=FAKE, seed=1, T=1.0, B=2, L=8, K=8,
+             d=4096, V=126464, acc=FAKE, cor=None, ra=None, rr=None, ws=FAKE, ws_bytes=1 << 20)
+    a.update(kw)
+    st = brisk.lib().brisk_spec_verify(a["hv"], a["W"], a["prop"], a["cid"], a["cpr"], a["u"], a["seed"],
+                                       a["T"], a["B"], a["L"], a["K"], a["d"], a["V"], a["acc"], a["cor"],
+                                       a["ra"], a["rr"], a["ws"], a["ws_bytes"], None)
     assert st == want
