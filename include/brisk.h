@@ -229,7 +229,9 @@ int brisk_spec_verify_workspace_size(int32_t B, int32_t L, int32_t V, int32_t K,
  *   lm_head     [V, d]   bf16
  *   proposal    [B, L]   int32   x
  *   cand_id     [B*L, K] int32   distinct candidate ids of each position
- *   cand_prob   [B*L, K] fp32    pi over those ids (tokens outside have pi = 0)
+ *   cand_prob   [B*L, K] fp32    pi over those ids (tokens outside have pi = 0);
+ *               nullable: NULL means the greedy proposer, pi = point mass at
+ *               x (when x is among the candidates)
  *   u_accept    [B*L]    fp32    uniforms in [0, 1) for the accept tests
  *   seed        key of the Philox4x32-10 generator of the residual draws
  *               (Gumbel variate of token v at row r from word v mod 4 of

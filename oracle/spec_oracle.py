@@ -28,8 +28,10 @@ G = -log(-log U).
 Readings (also in the design notes): R21 p_i is the verifier softmax at
 temperature T over the whole vocabulary; R22 pi_i is given as probabilities
 over the position's candidate ids (a token outside the candidates has
-pi = 0); R23 accept when u_i < min{1, p_i(x_i) / pi_i(x_i)}; R24 a fully
-accepted block has no correction (-1), as in the greedy rule.
+pi = 0); when none are given, the proposer is the greedy selection of
+Section 3.3, whose law is the point mass at x_i (if x_i is a candidate);
+R23 accept when u_i < min{1, p_i(x_i) / pi_i(x_i)}; R24 a fully accepted
+block has no correction (-1), as in the greedy rule.
 
 Parity pins: the committed token's distribution equals p_i (chi-square over
 many seeded trials, for a one-hot and a spread proposal law); acceptance
@@ -91,17 +93,20 @@ def spec_rows(logits: np.ndarray, T: float, x: np.ndarray, cand_id: np.ndarray, 
 
     ``logits`` [rows, V] are the verifier's logits (float32 values), ``x``
     [rows] the proposals, ``cand_id`` / ``cand_prob`` [rows, K] the proposal
-    law, ``u`` [rows] the accept uniforms.  ``row_ids`` are the generator row
-    indices (default 0..rows-1).
+    law (``cand_prob=None``: point mass at x among the candidates), ``u``
+    [rows] the accept uniforms.  ``row_ids`` are the generator row indices
+    (default 0..rows-1).
     """
     rows, V = logits.shape
     logp = verifier_log_probs(logits, T)
     p = np.exp(logp)
     pi = np.zeros((rows, V), dtype=np.float64)
     K = cand_id.shape[1]
-    np.add.at(pi, (np.repeat(np.arange(rows), K), cand_id.reshape(-1)),
-              np.asarray(cand_prob, dtype=np.float64).reshape(-1))
     ar = np.arange(rows)
+    if cand_prob is None:
+        cand_prob = (cand_id == np.asarray(x)[:, None]).astype(np.float64)
+    np.add.at(pi, (np.repeat(ar, K), cand_id.reshape(-1)),
+              np.asarray(cand_prob, dtype=np.float64).reshape(-1))
     px, pix = p[ar, x], pi[ar, x]
     ratio = np.where(pix > 0, px / np.where(pix > 0, pix, 1.0), np.inf)
     accept = u < np.minimum(1.0, ratio)

@@ -395,16 +395,18 @@ def corrector_loss(ver_hidden: torch.Tensor, lm_head: torch.Tensor, cand_id: tor
 
 
 def spec_verify(ver_hidden: torch.Tensor, lm_head: torch.Tensor, proposal: torch.Tensor,
-                cand_id: torch.Tensor, cand_prob: torch.Tensor, u_accept: torch.Tensor, seed: int,
+                cand_id: torch.Tensor, cand_prob: Optional[torch.Tensor], u_accept: torch.Tensor, seed: int,
                 temperature: float = 1.0, *, workspace: Optional[torch.Tensor] = None,
                 stream=None) -> Dict[str, torch.Tensor]:
     """Stochastic verification: ``accept_len``, ``correction`` [B] and the
-    per-position ``row_accept``, ``row_resample`` [B*L]."""
+    per-position ``row_accept``, ``row_resample`` [B*L].  ``cand_prob=None``
+    is the greedy proposer (pi = point mass at the proposal)."""
     _dev_tensor(ver_hidden, "ver_hidden", torch.bfloat16, 2)
     _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
     _dev_tensor(proposal, "proposal", torch.int32, 2)
     _dev_tensor(cand_id, "cand_id", torch.int32, 2)
-    _dev_tensor(cand_prob, "cand_prob", torch.float32, 2)
+    if cand_prob is not None:
+        _dev_tensor(cand_prob, "cand_prob", torch.float32, 2)
     _dev_tensor(u_accept, "u_accept", torch.float32, 1)
     B, L = proposal.shape
     K = cand_id.shape[1]

@@ -219,7 +219,7 @@ int brisk_spec_verify(const uint16_t* ver_hidden, const uint16_t* lm_head, const
                       uint64_t seed, float temperature, int32_t B, int32_t L, int32_t K, int32_t d,
                       int32_t V, int32_t* accept_len, int32_t* correction, int32_t* row_accept,
                       int32_t* row_resample, void* ws, size_t ws_bytes, void* stream) {
-  if (!proposal || !cand_id || !cand_prob || !u_accept || !accept_len) return BRISK_ERR_NULL;
+  if (!proposal || !cand_id || !u_accept || !accept_len) return BRISK_ERR_NULL;
   if (B < 1 || L < 1 || static_cast<int64_t>(B) * L > kMaxRows || K < 1 || K > 64 || V <= K ||
       !(temperature > 0.f) || temperature > 3.0e38f)
     return BRISK_ERR_SHAPE;

@@ -612,11 +612,17 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
   // pi_r nearly cancel, the residual weight needs every bit fp32 has
   const float lse = s_lse[0].x + logf(s_lse[0].y);
   const int32_t* ids = cand_id + static_cast<size_t>(row) * K;
-  const float* pis = cand_prob + static_cast<size_t>(row) * K;
+  // no cand_prob: the proposal is the greedy choice, pi_r = point mass at x_r
+  const float* pis = cand_prob ? cand_prob + static_cast<size_t>(row) * K : nullptr;
+  auto pi_of = [&](int k, int v) { return pis ? pis[k] : (v == x ? 1.f : 0.f); };
   float pi_x = 0.f;
-  for (int k = 0; k < K; ++k)
-    if (clamp_id(ids[k], V) == x) pi_x += pis[k];
-  const float p_x = expf(s_logit[K] * inv_T - lse);
+  for (int k = 0; k < K; ++k) {
+    const int v = clamp_id(ids[k], V);
+    if (v == x) pi_x += pi_of(k, v);
+  }
+  // p <= 1 holds exactly; the clamp keeps rounding (the dot products and the
+  // log-sum-exp add in different orders) from giving weight to pi = 1
+  const float p_x = fminf(1.f, expf(s_logit[K] * inv_T - lse));
   const bool accept = pi_x <= 0.f || u_accept[row] < fminf(1.f, p_x / pi_x);
   // residual draw: candidates from their exact weights, everyone else from
   // the best key (no candidate enters the lists; score s + G - lse)
@@ -624,7 +630,7 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
   int best_id = 0x7FFFFFFF;
   for (int k = 0; k < K; ++k) {
     const int v = clamp_id(ids[k], V);
-    const float w = expf(s_logit[k] * inv_T - lse) - pis[k];
+    const float w = fminf(1.f, expf(s_logit[k] * inv_T - lse)) - pi_of(k, v);
     if (w <= 0.f) continue;
     const uint4 g4 = philox4x32_10(make_uint4(static_cast<uint32_t>(v) >> 2, static_cast<uint32_t>(row), 0u, 0u),
                                    key0, key1);

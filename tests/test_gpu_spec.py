@@ -69,15 +69,17 @@ def _oracle_margins(logits, T, cid, prob, x, u, seed, row_ids):
     log p +- LOGP_ERR (and G +- G_ERR); a row is sure when the oracle's winner
     beats every other token over the whole interval.
     """
-    rs = oracle.spec_rows(logits, T, x, cid, prob.astype(np.float64), u.astype(np.float64), seed, row_ids)
+    pr = None if prob is None else prob.astype(np.float64)
+    rs = oracle.spec_rows(logits, T, x, cid, pr, u.astype(np.float64), seed, row_ids)
     ratio = np.where(rs["pi_x"] > 0, rs["p_x"] / np.maximum(rs["pi_x"], 1e-300), np.inf)
     lim = np.minimum(1.0, ratio)
     sure_a = np.abs(u - lim) > 2 * LOGP_ERR * np.where(np.isfinite(lim), lim, 1.0) + 1e-6
     lp = np.log(rs["p"])
     G = oracle.gumbel_for(row_ids, logits.shape[1], seed)
     with np.errstate(divide="ignore"):
-        lo = np.log(np.maximum(np.exp(lp - LOGP_ERR) - rs["pi"], 0.0)) + G - G_ERR
-        hi = np.log(np.maximum(np.exp(lp + LOGP_ERR) - rs["pi"], 0.0)) + G + G_ERR
+        # p <= 1 exactly, on both sides, so pi = 1 leaves no weight at all
+        lo = np.log(np.maximum(np.minimum(np.exp(lp - LOGP_ERR), 1.0) - rs["pi"], 0.0)) + G - G_ERR
+        hi = np.log(np.maximum(np.minimum(np.exp(lp + LOGP_ERR), 1.0) - rs["pi"], 0.0)) + G + G_ERR
     ar = np.arange(len(x))
     win = rs["resample"]
     hi_other = hi.copy()
@@ -119,6 +121,34 @@ def test_spec_decisions_match_oracle(name, T, law, n_sample):
         a = int(np.argmin(acc_rows[b])) if not acc_rows[b].all() else wl.L
         assert g["accept_len"][b] == a
         assert g["correction"][b] == (g["row_resample"][b * wl.L + a] if a < wl.L else -1)
+
+
+@pytest.mark.parametrize("name,T", [("tiny-d64-v512", 2.0), ("ragged-d200-v1003", 4.0), ("llada8b-b1-l32", 1.0)])
+def test_spec_greedy_proposer(name, T):
+    # cand_prob = NULL: the greedy proposer, pi = point mass at x; the result
+    # must equal an explicit one-hot law bit for bit, and the oracle
+    wl = _workload(name)
+    seed = 4242
+    blk, Hv, cid, _, _, u = _setup(wl, T, 17, "uniform")
+    x = cid[:, 0].reshape(wl.B, wl.L).astype(np.int32).copy()  # the top candidate
+    onehot = (cid == x.reshape(-1)[:, None]).astype(np.float32)
+    args = (Hv, blk.W, torch.from_numpy(x).cuda(), torch.from_numpy(cid).cuda())
+    ug = torch.from_numpy(u).cuda()
+    a = brisk.spec_verify(*args, None, ug, seed, T)
+    b = brisk.spec_verify(*args, torch.from_numpy(onehot).cuda(), ug, seed, T)
+    torch.cuda.synchronize()
+    for k in a:
+        assert torch.equal(a[k], b[k]), k
+    g = {k: v.cpu().numpy() for k, v in a.items()}
+    logits = oracle.lm_logits(oracle.bf16_to_f64(synth.bf16_bits(Hv)), synth.bf16_bits(blk.W))
+    sel = np.arange(wl.rows)
+    rs, sure_a, sure_r = _oracle_margins(logits, T, cid, None, x.reshape(-1), u, seed, sel)
+    assert sure_a.mean() > 0.9 and sure_r.mean() > 0.5, (sure_a.mean(), sure_r.mean())
+    assert np.array_equal(g["row_accept"][sure_a].astype(bool), rs["accept"][sure_a])
+    assert np.array_equal(g["row_resample"][sure_r], rs["resample"][sure_r])
+    # a rejected proposal is never drawn again at its own position
+    rej = g["row_accept"] == 0
+    assert not np.any(g["row_resample"][rej] == x.reshape(-1)[rej])
 
 
 def _chi2(counts, probs):

@@ -98,3 +98,39 @@ def test_block_stops_at_first_rejection():
         a = int(np.argmin(acc)) if not acc.all() else L
         assert out["accept_len"][b] == a
         assert out["correction"][b] == (rows["resample"][b * L + a] if a < L else -1)
+
+
+@pytest.mark.parametrize("T", [1.0, 2.5])
+def test_greedy_proposer_point_mass(T):
+    # no proposal probabilities: the proposer is the greedy selection, its law
+    # the point mass at x; acceptance happens with probability p(x) and the
+    # committed token is still distributed as p
+    rng = np.random.default_rng(12)
+    V, n = 10, 200_000
+    logits = rng.standard_normal(V) * 1.2
+    cand = np.array([4, 0, 8])
+    x = np.full((n, 1), cand[1], np.int32)
+    u = rng.random((n, 1))
+    L = np.repeat(logits[None, :].astype(np.float32), n, axis=0)
+    cid = np.repeat(cand[None, :], n, axis=0).astype(np.int32)
+    out = oracle.spec_verify(L, T, x, cid, None, u, seed=77)
+    committed = np.where(out["accept_len"] == 1, x[:, 0], out["correction"])
+    p = np.exp(oracle.verifier_log_probs(logits[None, :].astype(np.float32), T)[0])
+    assert _chi2(np.bincount(committed, minlength=V), p) > CHI_P
+    rate = p[cand[1]]
+    acc = (out["accept_len"] == 1).mean()
+    assert abs(acc - rate) < 5 * np.sqrt(rate * (1 - rate) / n)
+    # a rejected position never commits the proposal again
+    assert not np.any(out["correction"][out["accept_len"] == 0] == cand[1])
+
+
+def test_greedy_mode_equals_explicit_point_mass():
+    rng = np.random.default_rng(13)
+    rows, V, K = 64, 30, 5
+    logits = rng.standard_normal((rows, V)).astype(np.float32) * 2
+    cid = np.stack([rng.choice(V, K, replace=False) for _ in range(rows)]).astype(np.int32)
+    x = cid[np.arange(rows), rng.integers(0, K, rows)]
+    u = rng.random(rows)
+    a = oracle.spec_rows(logits, 1.3, x, cid, None, u, 5)
+    b = oracle.spec_rows(logits, 1.3, x, cid, (cid == x[:, None]).astype(np.float64), u, 5)
+    assert np.array_equal(a["accept"], b["accept"]) and np.array_equal(a["resample"], b["resample"])
