@@ -119,6 +119,22 @@ int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head,
                         float* cand_logit, int32_t* cand_id,
                         void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * The two launches of brisk_propose_block, one call each (same section of the
+ * paper, same arguments, limits and workspace).  brisk_propose_lmhead is the
+ * LM-head pass: it leaves in ws, for every row and vocabulary share, the
+ * ordered keys of that share's K largest logits.  brisk_propose_merge reduces
+ * those keys to the candidates.  brisk_propose_block is exactly the two in
+ * order on one stream; calling them separately lets a caller time or
+ * schedule each launch on its own.  A merge reads the workspace of the pass
+ * before it on the same stream, which must have used the same rows, V and K
+ * (the layout depends on them); it does not check that.
+ */
+int brisk_propose_lmhead(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
+                         int32_t V, int32_t K, void* ws, size_t ws_bytes, void* stream);
+int brisk_propose_merge(int32_t rows, int32_t V, int32_t K, float* cand_logit, int32_t* cand_id,
+                        const void* ws, size_t ws_bytes, void* stream);
+
 /* Workspace bytes brisk_rerank needs (written to *bytes). */
 int brisk_rerank_workspace_size(const brisk_corrector* c, int32_t B, int32_t L, int32_t K,
                                 size_t* bytes);

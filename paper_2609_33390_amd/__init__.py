@@ -28,13 +28,14 @@ from typing import Dict, Optional, Tuple
 
 import torch
 
-__all__ = ["BriskError", "Corrector", "propose_block", "rerank", "verify_accept", "accept_profile",
+__all__ = ["BriskError", "Corrector", "propose_block", "propose_lmhead", "propose_merge", "rerank", "verify_accept", "accept_profile",
            "propose_verify", "verify_commit", "corrector_loss", "spec_verify",
            "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
 ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
-               "brisk_propose_block", "brisk_rerank_workspace_size", "brisk_rerank",
+               "brisk_propose_block", "brisk_propose_lmhead", "brisk_propose_merge",
+               "brisk_rerank_workspace_size", "brisk_rerank",
                "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
                "brisk_verify_commit", "brisk_spec_verify_workspace_size", "brisk_spec_verify",
                "brisk_corrector_loss", "brisk_accept_profile_workspace_size",
@@ -81,6 +82,10 @@ def lib() -> ctypes.CDLL:
             L.brisk_propose_workspace_size.argtypes = [_i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
             L.brisk_propose_block.restype = ctypes.c_int
             L.brisk_propose_block.argtypes = [_p, _p, _i32, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
+            L.brisk_propose_lmhead.restype = ctypes.c_int
+            L.brisk_propose_lmhead.argtypes = [_p, _p, _i32, _i32, _i32, _i32, _p, _sz, _p]
+            L.brisk_propose_merge.restype = ctypes.c_int
+            L.brisk_propose_merge.argtypes = [_i32, _i32, _i32, _p, _p, _p, _sz, _p]
             L.brisk_rerank_workspace_size.restype = ctypes.c_int
             L.brisk_rerank_workspace_size.argtypes = [ctypes.POINTER(_CorrectorC), _i32, _i32, _i32,
                                                       ctypes.POINTER(_sz)]
@@ -196,6 +201,32 @@ def propose_block(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, *,
                                    _stream_ptr(dev, stream))
     _check(st, "brisk_propose_block")
     return cand_logit, cand_id
+
+
+def propose_lmhead(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, workspace: torch.Tensor, *,
+                   stream=None) -> None:
+    """The LM-head pass of propose_block alone: per-share ordered keys into ``workspace``."""
+    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
+    rows, d = hidden.shape
+    V = lm_head.shape[0]
+    if lm_head.shape[1] != d:
+        raise ValueError("hidden and lm_head disagree on d")
+    st = lib().brisk_propose_lmhead(_ptr(hidden), _ptr(lm_head), rows, d, V, K, _ptr(workspace),
+                                    workspace.numel() * workspace.element_size(),
+                                    _stream_ptr(hidden.device, stream))
+    _check(st, "brisk_propose_lmhead")
+
+
+def propose_merge(rows: int, V: int, K: int, workspace: torch.Tensor, cand_logit: torch.Tensor,
+                  cand_id: torch.Tensor, *, stream=None) -> None:
+    """The merge of propose_block alone: candidates from the keys a propose_lmhead left."""
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
+    st = lib().brisk_propose_merge(rows, V, K, _ptr(cand_logit), _ptr(cand_id), _ptr(workspace),
+                                   workspace.numel() * workspace.element_size(),
+                                   _stream_ptr(cand_logit.device, stream))
+    _check(st, "brisk_propose_merge")
 
 
 # ----------------------------------------------------------------- rerank

@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 5;
+constexpr int kAbiVersion = 6;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 
@@ -107,6 +107,30 @@ int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head, int32_t
   if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
   brisk::launch_propose(hidden, lm_head, rows, d, V, K, rows, cand_logit, cand_id, nullptr, ws,
                         static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_propose_lmhead(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
+                         int32_t V, int32_t K, void* ws, size_t ws_bytes, void* stream) {
+  const int st = lmhead_check(hidden, lm_head, rows, d, V, K);
+  if (st != BRISK_OK) return st;
+  const size_t need = brisk::propose_workspace_bytes(rows, V, K);
+  if (ws_bytes < need || (need > 0 && !ws)) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_propose_pass(hidden, lm_head, rows, d, V, K, ws, static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_propose_merge(int32_t rows, int32_t V, int32_t K, float* cand_logit, int32_t* cand_id,
+                        const void* ws, size_t ws_bytes, void* stream) {
+  if (!cand_logit || !cand_id) return BRISK_ERR_NULL;
+  if (rows < 1 || rows > kMaxRows || K < 1 || K > 64 || V < K) return BRISK_ERR_SHAPE;
+  if (!aligned4(cand_logit) || !aligned4(cand_id)) return BRISK_ERR_UNSUPPORTED;
+  const size_t need = brisk::propose_workspace_bytes(rows, V, K);
+  if (ws_bytes < need || (need > 0 && !ws)) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_propose_merge(rows, V, K, rows, cand_logit, cand_id, nullptr, ws,
+                              static_cast<hipStream_t>(stream));
   return launch_status();
 }
 

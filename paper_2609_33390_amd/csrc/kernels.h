@@ -13,6 +13,12 @@ namespace brisk {
 size_t propose_workspace_bytes(int rows, int V, int K);
 // rows = proposal rows (K candidates each) followed by verifier rows (argmax
 // each): rows_prop of them are proposal rows.
+// The two launches of launch_propose: the LM-head pass (per-group ordered
+// keys into ws) and the merge of those keys into candidates.
+void launch_propose_pass(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K, void* ws,
+                         hipStream_t s);
+void launch_propose_merge(int rows, int V, int K, int rows_prop, float* cand_logit, int32_t* cand_id,
+                          int32_t* ver_token, const void* ws, hipStream_t s);
 void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
                     int rows_prop, float* cand_logit, int32_t* cand_id, int32_t* ver_token,
                     void* ws, hipStream_t s);

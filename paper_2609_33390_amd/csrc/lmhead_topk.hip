@@ -43,7 +43,16 @@ struct TileCfg {
   // The epilogue reuses the stage buffer of the slice just consumed when it
   // fits (no copy targets that buffer until the next slice begins).
   static constexpr bool EPI_ALIAS = EPI_BYTES <= STAGE_BYTES;
-  static constexpr int LDS_BYTES = STAGES * STAGE_BYTES + (EPI_ALIAS ? 0 : EPI_BYTES);
+  // Small row tiles defer a tile's top-K into the next tile's reduction
+  // loop: the whole tile of logits waits in its own buffer, [TV][BR][EPI_V]
+  // fp32, while the copies of the next tile stream.
+  static constexpr bool DEFER = BR <= 32;
+  static constexpr int DEF_BYTES = DEFER ? BR * BV * 4 : 0;
+  // the epilogue's list floors, [BR][TPP] fp32, follow the buffers (one
+  // LDS object for the whole kernel: a second one makes the compiler wait
+  // for every outstanding LDS copy before each LDS read)
+  static constexpr int THR_OFF = STAGES * STAGE_BYTES + (DEFER ? DEF_BYTES : (EPI_ALIAS ? 0 : EPI_BYTES));
+  static constexpr int LDS_BYTES = THR_OFF + NT * 4;
   static_assert(ROWS % (RPI * NW) == 0 && BV % RPI == 0, "DMA instructions must tile the stage");
   static_assert(WV % 16 == 0 && WR % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(NT % BR == 0 && (TPP & (TPP - 1)) == 0, "epilogue thread mapping");
@@ -90,6 +99,11 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   if (bid >= full) return bid;
   return (bid % NXCD) * per + bid / NXCD;
 }
+
+// Equal vocabulary shares for weight-streaming shapes, and list floors shared
+// among the epilogue threads of a row (both described where they are used).
+constexpr bool kEvenShares = true;
+constexpr bool kRowThreshold = true;  // applied where TPP <= 2 (see the epilogue)
 
 // Whether the per-position lists fit in LDS for the in-workgroup merge (the
 // stage buffers are idle by then).
@@ -145,9 +159,10 @@ __device__ __forceinline__ bool is_candidate(const SampleArgs& sa, uint64_t mask
 template <class C, int KP, bool SAMPLE = false>
 __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4, C::NW / 4))) void lmhead_topk_kernel(
     const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int rows, int d, int V,
-    int n_rtiles, int n_vtiles, int tiles_per_group, uint64_t* __restrict__ partial, int n_parts,
-    SampleArgs sa) {
+    int n_rtiles, int n_groups, int tiles_per_group, int even, uint64_t* __restrict__ partial,
+    int n_parts, SampleArgs sa) {
   __shared__ __align__(16) unsigned char smem[C::LDS_BYTES];
+  float* const s_thr = reinterpret_cast<float*>(smem + C::THR_OFF);  // list floors, [position][TPP]
 
   const int tid = threadIdx.x, lane = tid & 63;
   // the wave index is uniform per wave; saying so keeps LDS bases in scalars
@@ -157,18 +172,30 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   const int rt = logical % n_rtiles;
   const int group = logical / n_rtiles;
   const int r0 = rt * C::BR;
-  const int vt_begin = group * tiles_per_group;
-  const int n_tiles = min(tiles_per_group, n_vtiles - vt_begin);
+  // Vocabulary rows [vb, ve) of this group: runs of whole tiles, or (even)
+  // equal shares cut at multiples of 16, so that every compute unit streams
+  // the same number of rows; the last tile of a share is partly masked.
+  int vb, ve;
+  if (even) {
+    vb = group == 0 ? 0 : static_cast<int>(static_cast<long long>(group) * V / n_groups) & ~15;
+    ve = group + 1 == n_groups ? V : static_cast<int>(static_cast<long long>(group + 1) * V / n_groups) & ~15;
+  } else {
+    vb = group * tiles_per_group * C::BV;
+    ve = min(V, vb + tiles_per_group * C::BV);
+  }
+  const int n_tiles = (ve - vb + C::BV - 1) / C::BV;
   const int nk = (d + C::BK - 1) / C::BK;
   const int tail = (d % C::BK) / 8;  // valid chunks of the last slice (0: slice is full)
 
   // ---- copy issue: stage g = (tile g / nk, slice g % nk); past the end the
   // last slice is re-read so every wave issues the same number of copies.
-  // Buffer resources bound-check every copy: lm_head rows >= V and hidden
-  // rows >= rows read as zeros.  Byte offsets fit in 32 bits (checked on the
-  // host).
+  // Buffer resources bound-check every copy: the lm_head resource starts at
+  // row vb and ends at row ve, so rows past the group's share read as zeros
+  // without touching memory, and hidden rows >= rows read as zeros.  Byte
+  // offsets fit in 32 bits (checked on the host).
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(W), static_cast<short>(0), static_cast<int>(static_cast<unsigned>(V) * d * 2u), 0x00020000);
+      const_cast<uint16_t*>(W + static_cast<size_t>(vb) * d), static_cast<short>(0),
+      static_cast<int>(static_cast<unsigned>(ve - vb) * d * 2u), 0x00020000);
   const __amdgpu_buffer_rsrc_t rh = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(H), static_cast<short>(0), static_cast<int>(static_cast<unsigned>(rows) * d * 2u), 0x00020000);
   const unsigned row_bytes = static_cast<unsigned>(d) * 2u;
@@ -183,7 +210,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       tl = n_tiles - 1;
       kt = nk - 1;
     }
-    const unsigned v0 = static_cast<unsigned>((vt_begin + tl) * C::BV), k0b = static_cast<unsigned>(kt * C::BK) * 2u;
+    const unsigned v0 = static_cast<unsigned>(tl * C::BV), k0b = static_cast<unsigned>(kt * C::BK) * 2u;
     unsigned char* base = smem + (g % C::STAGES) * C::STAGE_BYTES;
 #pragma unroll
     for (int i = 0; i < C::NDMA; ++i) {
@@ -224,6 +251,59 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   if constexpr (SAMPLE) {
     if (row_ok) cmask = candidate_mask(sa, r0 + ep, V);
   }
+
+  // One float4 of staged logits (columns col..col+3 of chunk x) of this
+  // thread's position folded into its list.
+  auto consume = [&](const float* buf, int x, int col, int v0) {
+    floatx4 v = *reinterpret_cast<const floatx4*>(buf + ep * C::EPI_V + epi_slot(ep, col >> 2) * 4);
+    const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);  // a multiple of 4
+    if constexpr (SAMPLE) {
+      float m4 = -INFINITY;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        v[q] *= sa.inv_T;
+        if (vid0 + q < ve) m4 = fmaxf(m4, v[q]);
+      }
+      if (m4 > lse_m) {
+        lse_s *= __expf(lse_m - m4);
+        lse_m = m4;
+      }
+      const uint4 w = philox4x32_10(make_uint4(static_cast<uint32_t>(vid0) >> 2, static_cast<uint32_t>(r0 + ep), 0u, 0u),
+                                    sa.key0, sa.key1);
+      const uint32_t wq[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (vid0 + q < ve) lse_s += __expf(v[q] - lse_m);
+        v[q] += gumbel_of(wq[q]);
+      }
+    }
+    // common case: none of the four logits reaches the list's smallest
+    // entry, which one float compare decides; only then build keys
+    const float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+    if (m >= thr) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int vid = vid0 + q;
+        const uint64_t key = make_key(v[q], static_cast<uint32_t>(vid));
+        if (vid < ve && v[q] >= thr && key > list[KP - 1]) {
+          // sampling keeps candidates out: their draws use exact weights
+          if constexpr (SAMPLE) {
+            if (!row_ok || is_candidate(sa, cmask, r0 + ep, vid, V)) continue;
+          }
+          list_insert(list, key);
+        }
+      }
+      thr = fmaxf(thr, list_floor(list[KP - 1]));
+    }
+  };
+  // deferred top-K: item i is float4 (i % kColFull) of chunk i / kColFull
+  constexpr int kItems = C::TV * kColFull;
+  float* const sD = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
+  int pend = kItems, pend_v0 = 0;
+  auto consume_item = [&](int i) {
+    const int x = i / kColFull;
+    consume(sD + x * C::BR * C::EPI_V, x, esub * 4 + (i % kColFull) * C::TPP * 4, pend_v0);
+  };
 
   floatx4 acc[C::TV][C::TR];
 #pragma unroll
@@ -270,12 +350,37 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         __builtin_amdgcn_sched_group_barrier(0x100, C::TV + C::TR, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, C::TV * C::TR, 0);
       }
+      if constexpr (C::DEFER) {
+        // the previous tile's top-K, spread evenly over this tile's slices
+        while (pend < kItems && kt * kItems >= pend * nk) consume_item(pend++);
+      }
     }
 
     // Fused top-K over this tile.  Chunk x stages accumulator block x of
     // every wave as fp32 [position][wave_v * 16 + column]; each thread then
     // folds its position's columns into its running list.
-    const int v0 = (vt_begin + tl) * C::BV;
+    const int v0 = vb + tl * C::BV;
+    if constexpr (C::DEFER) {
+      while (pend < kItems) consume_item(pend++);  // tiles shorter than kItems slices
+      lds_sync();  // every thread has finished with the previous tile's logits
+#pragma unroll
+      for (int x = 0; x < C::TV; ++x) {
+#pragma unroll
+        for (int y = 0; y < C::TR; ++y) {
+          const int p = wr * C::WR + y * 16 + l15;
+          *reinterpret_cast<floatx4*>(sD + (x * C::BR + p) * C::EPI_V + epi_slot(p, wv * 4 + (lane >> 4)) * 4) =
+              acc[x][y];
+          acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+        }
+      }
+      lds_sync();
+      pend = 0;
+      pend_v0 = v0;
+      if (tl == n_tiles - 1) {
+        while (pend < kItems) consume_item(pend++);
+      }
+      continue;
+    }
     float* sE;
     if constexpr (C::EPI_ALIAS) {
       sE = reinterpret_cast<float*>(smem + ((tl * nk + nk - 1) % C::STAGES) * C::STAGE_BYTES);
@@ -293,50 +398,18 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       }
       lds_sync();
 #pragma unroll kColUnroll
-      for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) {
-        floatx4 v = *reinterpret_cast<const floatx4*>(sE + ep * C::EPI_V + epi_slot(ep, col >> 2) * 4);
-        if constexpr (SAMPLE) {
-          const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);  // a multiple of 4
-          float m4 = -INFINITY;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            v[q] *= sa.inv_T;
-            if (vid0 + q < V) m4 = fmaxf(m4, v[q]);
-          }
-          if (m4 > lse_m) {
-            lse_s *= __expf(lse_m - m4);
-            lse_m = m4;
-          }
-          const uint4 w = philox4x32_10(make_uint4(static_cast<uint32_t>(vid0) >> 2, static_cast<uint32_t>(r0 + ep), 0u, 0u),
-                                        sa.key0, sa.key1);
-          const uint32_t wq[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            if (vid0 + q < V) lse_s += __expf(v[q] - lse_m);
-            v[q] += gumbel_of(wq[q]);
-          }
-        }
-        // common case: none of the four logits reaches the list's smallest
-        // entry, which one float compare decides; only then build keys
-        const float m = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
-        if (m >= thr) {
-          const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int vid = vid0 + q;
-            const uint64_t key = make_key(v[q], static_cast<uint32_t>(vid));
-            if (vid < V && key > list[KP - 1]) {
-              // sampling keeps candidates out: their draws use exact weights
-              if constexpr (SAMPLE) {
-                if (!row_ok || is_candidate(sa, cmask, r0 + ep, vid, V)) continue;
-              }
-              list_insert(list, key);
-            }
-          }
-          thr = list_floor(list[KP - 1]);
-        }
-      }
+      for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) consume(sE, x, col, v0);
+      // Share the floors of a row's TPP lists: each thread's floor bounds the
+      // row's KP-th largest key from below, so the largest of them filters
+      // every list of the row.  It pays on the large-row tile (two lists per
+      // row, long streams); with eight lists per row and short streams the
+      // exchange costs more than the insertions it saves.
+      if constexpr (kRowThreshold && C::TPP == 2) s_thr[ep * C::TPP + esub] = thr;
       lds_sync();
+      if constexpr (kRowThreshold && C::TPP == 2) {
+#pragma unroll
+        for (int e = 0; e < C::TPP; ++e) thr = fmaxf(thr, s_thr[ep * C::TPP + e]);
+      }
     }
   }
   stage_sync<0>();  // the trailing copies have landed; LDS is free
@@ -487,6 +560,7 @@ constexpr int kTargetWorkgroups = 256;  // one persistent workgroup per compute 
 struct Plan {
   int cfg;  // 0 small, 1 mid, 2 large
   int n_rtiles, n_vtiles, tiles_per_group, n_groups, n_parts, KP;
+  int even;  // equal vocabulary shares instead of runs of whole tiles
 };
 
 template <class C>
@@ -499,6 +573,17 @@ Plan make_plan_for(int cfg, int rows, int V, int K) {
   want = want < 1 ? 1 : (want > p.n_vtiles ? p.n_vtiles : want);
   p.tiles_per_group = (p.n_vtiles + want - 1) / want;
   p.n_groups = (p.n_vtiles + p.tiles_per_group - 1) / p.tiles_per_group;
+  // Weight-streaming shapes: when runs of whole tiles leave compute units
+  // idle, cut the vocabulary into one equal share per compute unit instead
+  // (the partly masked last tile costs MFMA time, which these shapes have
+  // to spare, but no memory traffic).
+  const int want_all = kTargetWorkgroups / p.n_rtiles < 1 ? 1 : kTargetWorkgroups / p.n_rtiles;
+  p.even = 0;
+  if (kEvenShares && cfg != 2 && p.n_groups < want_all && V / want_all >= C::BV / 2) {
+    p.even = 1;
+    p.n_groups = want_all;
+    p.tiles_per_group = (V / want_all + 16 + C::BV - 1) / C::BV;
+  }
   p.KP = K <= 4 ? 4 : K <= 8 ? 8 : K <= 16 ? 16 : K <= 32 ? 32 : 64;
   const bool wg_merge = p.KP == 4    ? kWgMerge<C, 4>
                         : p.KP == 8  ? kWgMerge<C, 8>
@@ -520,7 +605,7 @@ void launch_tile(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, 
                  uint64_t* partial, hipStream_t s, SampleArgs sa = SampleArgs{}) {
   const int nblocks = p.n_rtiles * p.n_groups;
   hipLaunchKernelGGL((lmhead_topk_kernel<C, KP, SAMPLE>), dim3(nblocks), dim3(C::NT), 0, s, H, W, rows,
-                     d, V, p.n_rtiles, p.n_vtiles, p.tiles_per_group, partial, p.n_parts, sa);
+                     d, V, p.n_rtiles, p.n_groups, p.tiles_per_group, p.even, partial, p.n_parts, sa);
 }
 
 // ---------------------------------------------------------------------------
@@ -678,14 +763,18 @@ __global__ __launch_bounds__(256) void spec_commit_kernel(const int32_t* __restr
 }
 
 template <int KP>
-void launch_kp(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
-               int rows_prop, uint64_t* partial, float* cand_logit, int32_t* cand_id,
-               int32_t* ver_token, hipStream_t s) {
+void launch_kp_pass(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, int d, int V,
+                    uint64_t* partial, hipStream_t s) {
   switch (p.cfg) {
     case 0: launch_tile<SmallRows, KP>(p, H, W, rows, d, V, partial, s); break;
     case 1: launch_tile<MidRows, KP>(p, H, W, rows, d, V, partial, s); break;
     default: launch_tile<LargeRows, KP>(p, H, W, rows, d, V, partial, s); break;
   }
+}
+
+template <int KP>
+void launch_kp_merge(const Plan& p, int rows, int K, int rows_prop, const uint64_t* partial,
+                     float* cand_logit, int32_t* cand_id, int32_t* ver_token, hipStream_t s) {
   hipLaunchKernelGGL((topk_merge_kernel<KP>), dim3(rows), dim3(256), 0, s, partial, rows,
                      p.n_parts * KP, K, rows_prop, cand_logit, cand_id, ver_token);
 }
@@ -751,18 +840,37 @@ size_t propose_workspace_bytes(int rows, int V, int K) {
   return static_cast<size_t>(rows) * p.n_parts * p.KP * sizeof(uint64_t);
 }
 
-void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
-                    int rows_prop, float* cand_logit, int32_t* cand_id, int32_t* ver_token,
-                    void* ws, hipStream_t s) {
+void launch_propose_pass(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K, void* ws,
+                         hipStream_t s) {
   const Plan p = make_plan(rows, V, K);
   uint64_t* partial = static_cast<uint64_t*>(ws);
   switch (p.KP) {
-    case 4: launch_kp<4>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
-    case 8: launch_kp<8>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
-    case 16: launch_kp<16>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
-    case 32: launch_kp<32>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
-    default: launch_kp<64>(p, H, W, rows, d, V, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    case 4: launch_kp_pass<4>(p, H, W, rows, d, V, partial, s); break;
+    case 8: launch_kp_pass<8>(p, H, W, rows, d, V, partial, s); break;
+    case 16: launch_kp_pass<16>(p, H, W, rows, d, V, partial, s); break;
+    case 32: launch_kp_pass<32>(p, H, W, rows, d, V, partial, s); break;
+    default: launch_kp_pass<64>(p, H, W, rows, d, V, partial, s); break;
   }
+}
+
+void launch_propose_merge(int rows, int V, int K, int rows_prop, float* cand_logit, int32_t* cand_id,
+                          int32_t* ver_token, const void* ws, hipStream_t s) {
+  const Plan p = make_plan(rows, V, K);
+  const uint64_t* partial = static_cast<const uint64_t*>(ws);
+  switch (p.KP) {
+    case 4: launch_kp_merge<4>(p, rows, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    case 8: launch_kp_merge<8>(p, rows, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    case 16: launch_kp_merge<16>(p, rows, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    case 32: launch_kp_merge<32>(p, rows, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+    default: launch_kp_merge<64>(p, rows, K, rows_prop, partial, cand_logit, cand_id, ver_token, s); break;
+  }
+}
+
+void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
+                    int rows_prop, float* cand_logit, int32_t* cand_id, int32_t* ver_token,
+                    void* ws, hipStream_t s) {
+  launch_propose_pass(H, W, rows, d, V, K, ws, s);
+  launch_propose_merge(rows, V, K, rows_prop, cand_logit, cand_id, ver_token, ws, s);
 }
 
 }  // namespace brisk

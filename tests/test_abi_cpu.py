@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 5
+    assert L.brisk_abi_version() == 6
     for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5):
         assert L.brisk_status_str(st).decode()
     assert L.brisk_status_str(123).decode() == "unknown status"
@@ -62,6 +62,30 @@ def _propose(**kw):
 ])
 def test_propose_validation(kw, want):
     assert _propose(**kw) == want
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(hidden=None), ENULL), (dict(lm_head=None), ENULL), (dict(rows=0), ESHAPE), (dict(K=65), ESHAPE),
+    (dict(V=4, K=8), ESHAPE), (dict(d=4100), EUNSUP), (dict(hidden=MISALIGNED), EUNSUP),
+    (dict(ws_bytes=0), EWS), (dict(ws=None, ws_bytes=1 << 40), EWS), (dict(ws=MISALIGNED), EUNSUP),
+])
+def test_propose_lmhead_validation(kw, want):
+    a = dict(hidden=FAKE, lm_head=FAKE, rows=32, d=4096, V=126464, K=8, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    assert brisk.lib().brisk_propose_lmhead(a["hidden"], a["lm_head"], a["rows"], a["d"], a["V"], a["K"],
+                                            a["ws"], a["ws_bytes"], None) == want
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(cl=None), ENULL), (dict(ci=None), ENULL), (dict(rows=0), ESHAPE), (dict(K=0), ESHAPE),
+    (dict(V=4, K=8), ESHAPE), (dict(ci=MISALIGNED), EUNSUP), (dict(ws_bytes=0), EWS),
+    (dict(ws=MISALIGNED), EUNSUP),
+])
+def test_propose_merge_validation(kw, want):
+    a = dict(rows=32, V=126464, K=8, cl=FAKE, ci=FAKE, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    assert brisk.lib().brisk_propose_merge(a["rows"], a["V"], a["K"], a["cl"], a["ci"], a["ws"],
+                                           a["ws_bytes"], None) == want
 
 
 def test_propose_workspace_size_query():

@@ -141,6 +141,9 @@ RAGGED = [
     # rows, d, V, K: tails in every tiled dimension
     (1, 64, 256, 1), (7, 72, 1000, 5), (33, 136, 777, 16), (65, 200, 2049, 8),
     (130, 64, 4100, 33), (300, 520, 3000, 64), (32, 4096, 513, 4),
+    # vocabularies large enough for one equal share per compute unit (shares
+    # of 130-160 rows cut at multiples of 16, partly masked tiles)
+    (5, 72, 33333, 7), (50, 136, 40961, 16), (20, 64, 36001, 64),
 ]
 
 
