@@ -183,16 +183,20 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     vb = group * tiles_per_group * C::BV;
     ve = min(V, vb + tiles_per_group * C::BV);
   }
+  // Tiles of the share: runs of BV rows, the last one partial.  (A short
+  // extra tile at the end, to shorten the top-K that cannot overlap with
+  // copies, costs more: a slice takes time whether or not its rows exist.)
   const int n_tiles = (ve - vb + C::BV - 1) / C::BV;
+  auto tile_start = [&](int t) { return vb + t * C::BV; };
+  auto tile_end = [&](int t) { return min(ve, vb + (t + 1) * C::BV); };
   const int nk = (d + C::BK - 1) / C::BK;
   const int tail = (d % C::BK) / 8;  // valid chunks of the last slice (0: slice is full)
 
-  // ---- copy issue: stage g = (tile g / nk, slice g % nk); past the end the
-  // last slice is re-read so every wave issues the same number of copies.
-  // Buffer resources bound-check every copy: the lm_head resource starts at
-  // row vb and ends at row ve, so rows past the group's share read as zeros
-  // without touching memory, and hidden rows >= rows read as zeros.  Byte
-  // offsets fit in 32 bits (checked on the host).
+  // ---- copy issue: stage g = (tile g / nk, slice g % nk); nothing past the
+  // last slice.  Buffer resources bound-check every copy: the lm_head
+  // resource starts at row vb and ends at row ve, so rows past the group's
+  // share read as zeros without touching memory, and hidden rows >= rows
+  // read as zeros.  Byte offsets fit in 32 bits (checked on the host).
   const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(W + static_cast<size_t>(vb) * d), static_cast<short>(0),
       static_cast<int>(static_cast<unsigned>(ve - vb) * d * 2u), 0x00020000);
@@ -205,11 +209,8 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   const unsigned lane_voff = static_cast<unsigned>(lane / C::CPR) * row_bytes +
                              static_cast<unsigned>(swz<C::CPR>(lane / C::CPR, lane % C::CPR)) * 16u;
   auto issue = [&](int g) {
-    int tl = g / nk, kt = g % nk;
-    if (tl >= n_tiles) {
-      tl = n_tiles - 1;
-      kt = nk - 1;
-    }
+    const int tl = g / nk, kt = g % nk;
+    if (tl >= n_tiles) return;
     const unsigned v0 = static_cast<unsigned>(tl * C::BV), k0b = static_cast<unsigned>(kt * C::BK) * 2u;
     unsigned char* base = smem + (g % C::STAGES) * C::STAGE_BYTES;
 #pragma unroll
@@ -254,15 +255,16 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
 
   // One float4 of staged logits (columns col..col+3 of chunk x) of this
   // thread's position folded into its list.
-  auto consume = [&](const float* buf, int x, int col, int v0) {
-    floatx4 v = *reinterpret_cast<const floatx4*>(buf + ep * C::EPI_V + epi_slot(ep, col >> 2) * 4);
+  auto consume = [&](const float* buf, int x, int col, int v0, int vend) {
     const int vid0 = v0 + (col >> 4) * C::WV + x * 16 + (col & 15);  // a multiple of 4
+    if (vid0 >= vend) return;  // columns past the tile's last row
+    floatx4 v = *reinterpret_cast<const floatx4*>(buf + ep * C::EPI_V + epi_slot(ep, col >> 2) * 4);
     if constexpr (SAMPLE) {
       float m4 = -INFINITY;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         v[q] *= sa.inv_T;
-        if (vid0 + q < ve) m4 = fmaxf(m4, v[q]);
+        if (vid0 + q < vend) m4 = fmaxf(m4, v[q]);
       }
       if (m4 > lse_m) {
         lse_s *= __expf(lse_m - m4);
@@ -273,7 +275,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       const uint32_t wq[4] = {w.x, w.y, w.z, w.w};
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        if (vid0 + q < ve) lse_s += __expf(v[q] - lse_m);
+        if (vid0 + q < vend) lse_s += __expf(v[q] - lse_m);
         v[q] += gumbel_of(wq[q]);
       }
     }
@@ -285,7 +287,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       for (int q = 0; q < 4; ++q) {
         const int vid = vid0 + q;
         const uint64_t key = make_key(v[q], static_cast<uint32_t>(vid));
-        if (vid < ve && v[q] >= thr && key > list[KP - 1]) {
+        if (vid < vend && v[q] >= thr && key > list[KP - 1]) {
           // sampling keeps candidates out: their draws use exact weights
           if constexpr (SAMPLE) {
             if (!row_ok || is_candidate(sa, cmask, r0 + ep, vid, V)) continue;
@@ -299,10 +301,10 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   // deferred top-K: item i is float4 (i % kColFull) of chunk i / kColFull
   constexpr int kItems = C::TV * kColFull;
   float* const sD = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
-  int pend = kItems, pend_v0 = 0;
+  int pend = kItems, pend_v0 = 0, pend_end = 0;
   auto consume_item = [&](int i) {
     const int x = i / kColFull;
-    consume(sD + x * C::BR * C::EPI_V, x, esub * 4 + (i % kColFull) * C::TPP * 4, pend_v0);
+    consume(sD + x * C::BR * C::EPI_V, x, esub * 4 + (i % kColFull) * C::TPP * 4, pend_v0, pend_end);
   };
 
   floatx4 acc[C::TV][C::TR];
@@ -317,7 +319,10 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   for (int tl = 0; tl < n_tiles; ++tl) {
     for (int kt = 0; kt < nk; ++kt) {
       const int g = tl * nk + kt;
-      stage_sync<(C::STAGES - 2) * C::NDMA>();  // slice g landed; everyone is done with slice g-1
+      // slice g landed; everyone is done with slice g-1 (in the last slices
+      // fewer younger copies exist, so wait for all)
+      if (g + C::STAGES - 2 < n_tiles * nk) stage_sync<(C::STAGES - 2) * C::NDMA>();
+      else stage_sync<0>();
       issue(g + C::STAGES - 1);                  // refills the buffer slice g-1 used
       const unsigned char* sb = smem + (g % C::STAGES) * C::STAGE_BYTES;
       if (tail && kt == nk - 1) {
@@ -359,7 +364,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     // Fused top-K over this tile.  Chunk x stages accumulator block x of
     // every wave as fp32 [position][wave_v * 16 + column]; each thread then
     // folds its position's columns into its running list.
-    const int v0 = vb + tl * C::BV;
+    const int v0 = tile_start(tl), vend = tile_end(tl);
     if constexpr (C::DEFER) {
       while (pend < kItems) consume_item(pend++);  // tiles shorter than kItems slices
       lds_sync();  // every thread has finished with the previous tile's logits
@@ -376,6 +381,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       lds_sync();
       pend = 0;
       pend_v0 = v0;
+      pend_end = vend;
       if (tl == n_tiles - 1) {
         while (pend < kItems) consume_item(pend++);
       }
@@ -398,7 +404,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       }
       lds_sync();
 #pragma unroll kColUnroll
-      for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) consume(sE, x, col, v0);
+      for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) consume(sE, x, col, v0, vend);
       // Share the floors of a row's TPP lists: each thread's floor bounds the
       // row's KP-th largest key from below, so the largest of them filters
       // every list of the row.  It pays on the large-row tile (two lists per
