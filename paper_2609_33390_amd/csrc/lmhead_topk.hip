@@ -52,7 +52,13 @@ struct TileCfg {
   // LDS object for the whole kernel: a second one makes the compiler wait
   // for every outstanding LDS copy before each LDS read)
   static constexpr int THR_OFF = STAGES * STAGE_BYTES + (DEFER ? DEF_BYTES : (EPI_ALIAS ? 0 : EPI_BYTES));
-  static constexpr int LDS_BYTES = THR_OFF + NT * 4;
+  // Per-position thresholds, queue counters and an overflow flag of the
+  // filtered epilogue (see the kernel), after the floors.
+  static constexpr int POS_OFF = THR_OFF + NT * 4;
+  static constexpr int LDS_BYTES = POS_OFF + BR * 8 + 16;
+  // survivors a position's queue holds per tile (the queues use the stage
+  // buffer the epilogue aliases)
+  static constexpr int QCAP = STAGE_BYTES / (BR * 8);
   static_assert(ROWS % (RPI * NW) == 0 && BV % RPI == 0, "DMA instructions must tile the stage");
   static_assert(WV % 16 == 0 && WR % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(NT % BR == 0 && (TPP & (TPP - 1)) == 0, "epilogue thread mapping");
@@ -163,6 +169,15 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     int n_parts, SampleArgs sa) {
   __shared__ __align__(16) unsigned char smem[C::LDS_BYTES];
   float* const s_thr = reinterpret_cast<float*>(smem + C::THR_OFF);  // list floors, [position][TPP]
+  // Filtered epilogue (large-row tiles, plain pass): from the second tile on,
+  // each lane tests its own accumulators against its positions' thresholds
+  // (the largest list floor of the position, a lower bound of its KP-th
+  // largest key) and queues only the survivors, which the position's list
+  // owners then fold.  A tile whose queues overflow takes the full path.
+  constexpr bool kFilt = !SAMPLE && C::BR >= 128 && C::EPI_ALIAS && KP <= 8;  // more keys spill
+  float* const s_pthr = reinterpret_cast<float*>(smem + C::POS_OFF);        // [BR]
+  int* const s_cnt = reinterpret_cast<int*>(smem + C::POS_OFF + C::BR * 4);  // [BR]
+  int* const s_flag = reinterpret_cast<int*>(smem + C::POS_OFF + C::BR * 8);
 
   const int tid = threadIdx.x, lane = tid & 63;
   // the wave index is uniform per wave; saying so keeps LDS bases in scalars
@@ -307,6 +322,14 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     consume(sD + x * C::BR * C::EPI_V, x, esub * 4 + (i % kColFull) * C::TPP * 4, pend_v0, pend_end);
   };
 
+  if constexpr (kFilt) {
+    for (int i = tid; i < C::BR; i += C::NT) {
+      s_pthr[i] = -INFINITY;
+      s_cnt[i] = 0;
+    }
+    if (tid == 0) s_flag[0] = 0;  // first read after the pipeline's barriers
+  }
+
   floatx4 acc[C::TV][C::TR];
 #pragma unroll
   for (int a = 0; a < C::TV; ++a)
@@ -394,6 +417,56 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     } else {
       sE = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
     }
+    if constexpr (kFilt) {
+      if (tl > 0) {
+        // lane l holds, for position wr*WR + y*16 + l%16, the logits of
+        // vocabulary rows wv*WV + x*16 + 4*(l/16) + q of the tile
+        uint64_t* const sq = reinterpret_cast<uint64_t*>(sE);
+        float pt[C::TR];
+#pragma unroll
+        for (int y = 0; y < C::TR; ++y) pt[y] = s_pthr[wr * C::WR + y * 16 + l15];
+#pragma unroll
+        for (int x = 0; x < C::TV; ++x) {
+#pragma unroll
+          for (int y = 0; y < C::TR; ++y) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float v = acc[x][y][q];
+              const int vid = v0 + wv * C::WV + x * 16 + 4 * (lane >> 4) + q;
+              if (v >= pt[y] && vid < vend) {
+                const int p = wr * C::WR + y * 16 + l15;
+                const int idx = atomicAdd(&s_cnt[p], 1);
+                if (idx < C::QCAP) sq[p * C::QCAP + idx] = make_key(v, static_cast<uint32_t>(vid));
+                else s_flag[0] = 1;
+              }
+            }
+          }
+        }
+        lds_sync();
+        if (s_flag[0] == 0) {  // uniform: every thread reads the same flag
+          const int n = min(s_cnt[ep], C::QCAP);
+          for (int i = esub; i < n; i += C::TPP) {
+            const uint64_t key = sq[ep * C::QCAP + i];
+            if (key > list[KP - 1]) list_insert(list, key);
+          }
+          thr = fmaxf(thr, list_floor(list[KP - 1]));
+#pragma unroll
+          for (int x = 0; x < C::TV; ++x)
+#pragma unroll
+            for (int y = 0; y < C::TR; ++y) acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+          s_thr[ep * C::TPP + esub] = thr;
+          lds_sync();  // queues read, floors written
+#pragma unroll
+          for (int e = 0; e < C::TPP; ++e) thr = fmaxf(thr, s_thr[ep * C::TPP + e]);
+          if (esub == 0) {
+            s_pthr[ep] = thr;
+            s_cnt[ep] = 0;
+          }
+          continue;  // the next tile's slices begin with a barrier
+        }
+        // a queue overflowed: the whole tile takes the full path below
+      }
+    }
 #pragma unroll
     for (int x = 0; x < C::TV; ++x) {
 #pragma unroll
@@ -416,6 +489,15 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
 #pragma unroll
         for (int e = 0; e < C::TPP; ++e) thr = fmaxf(thr, s_thr[ep * C::TPP + e]);
       }
+    }
+    if constexpr (kFilt) {
+      // thresholds for the next tile; counters and flag cleared (read by
+      // every thread before the last barrier above)
+      if (esub == 0) {
+        s_pthr[ep] = thr;
+        s_cnt[ep] = 0;
+      }
+      if (tid == 0) s_flag[0] = 0;
     }
   }
   stage_sync<0>();  // the trailing copies have landed; LDS is free

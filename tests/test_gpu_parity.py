@@ -159,6 +159,26 @@ def test_propose_ragged(rows, d, V, K):
     check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
 
 
+@pytest.mark.parametrize("order", ["rising", "falling"])
+def test_propose_monotone_logits(order):
+    # 256 rows and V = 2^17 + 37: three vocabulary tiles per workgroup on the
+    # large-row tile.  Logits that rise with the token id make every later
+    # tile beat the thresholds of the earlier ones (the survivor queues
+    # overflow); falling logits leave later tiles with no survivors.
+    rows, d, V, K = 256, 64, (1 << 17) + 37, 8
+    g = torch.Generator(device="cpu").manual_seed(41)
+    u = torch.randn(d, generator=g)
+    u = u / u.norm()
+    H = (u[None, :] + 0.05 * torch.randn(rows, d, generator=g)).to(torch.bfloat16)
+    ramp = torch.linspace(-4.0, 4.0, V) if order == "rising" else torch.linspace(4.0, -4.0, V)
+    W = (ramp[:, None] * u[None, :] + 0.01 * torch.randn(V, d, generator=g)).to(torch.bfloat16)
+    cl, ci = brisk.propose_block(H.to(DEV), W.to(DEV), K)
+    torch.cuda.synchronize()
+    Hb, Wb = synth.bf16_bits(H), synth.bf16_bits(W)
+    ol = oracle.lm_logits(oracle.bf16_to_f64(Hb), Wb)
+    check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
+
+
 @pytest.mark.parametrize("B,L,K,d,V,r", [(3, 5, 5, 72, 1000, 32), (2, 9, 4, 136, 600, 96),
                                           (5, 3, 16, 64, 2000, 320), (70, 2, 8, 64, 512, 256)])
 def test_rerank_ragged(B, L, K, d, V, r):
