@@ -429,15 +429,18 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         for (int x = 0; x < C::TV; ++x) {
 #pragma unroll
           for (int y = 0; y < C::TR; ++y) {
+            const floatx4 a4 = acc[x][y];
+            // one compare per four logits decides the common case
+            if (fmaxf(fmaxf(a4[0], a4[1]), fmaxf(a4[2], a4[3])) >= pt[y]) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float v = acc[x][y][q];
-              const int vid = v0 + wv * C::WV + x * 16 + 4 * (lane >> 4) + q;
-              if (v >= pt[y] && vid < vend) {
-                const int p = wr * C::WR + y * 16 + l15;
-                const int idx = atomicAdd(&s_cnt[p], 1);
-                if (idx < C::QCAP) sq[p * C::QCAP + idx] = make_key(v, static_cast<uint32_t>(vid));
-                else s_flag[0] = 1;
+              for (int q = 0; q < 4; ++q) {
+                const int vid = v0 + wv * C::WV + x * 16 + 4 * (lane >> 4) + q;
+                if (a4[q] >= pt[y] && vid < vend) {
+                  const int p = wr * C::WR + y * 16 + l15;
+                  const int idx = atomicAdd(&s_cnt[p], 1);
+                  if (idx < C::QCAP) sq[p * C::QCAP + idx] = make_key(a4[q], static_cast<uint32_t>(vid));
+                  else s_flag[0] = 1;
+                }
               }
             }
           }
