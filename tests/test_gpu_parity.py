@@ -124,6 +124,21 @@ def test_full_workload(name):
 
 
 @pytest.mark.slow
+def test_full_workload_margin_scaled_planting():
+    """Planted targets with a margin of about 2-3 logits over the best random
+    token (boost 0.12 H/|H|, about 7.7 at d = 4096, against a largest random
+    logit near 5.6): the verifier's noise now disagrees at some positions, so
+    accept lengths spread, and every stage still matches the oracle."""
+    blk = synth.make_block("llada8b-b64-l32", DEV, plant_scale=0.12)
+    g = run_step(blk)
+    io = oracle_inputs(blk)
+    check_step(blk, g, io, sample_rows(blk.wl.rows))
+    hist = np.bincount(g["accept"], minlength=blk.wl.L + 1)
+    _say(f"  accept histogram {hist.tolist()}")
+    assert (g["accept"] < blk.wl.L).any() and len(np.unique(g["accept"])) >= 3
+
+
+@pytest.mark.slow
 def test_full_workload_scaled_corrector():
     """Flat rows with a strong corrector at the 7B wide-vocab shape: the rerank
     changes choices and still agrees with the oracle."""
