@@ -56,6 +56,11 @@ struct TileCfg {
   // filtered epilogue (see the kernel), after the floors.
   static constexpr int POS_OFF = THR_OFF + NT * 4;
   static constexpr int LDS_BYTES = POS_OFF + BR * 8 + 16;
+  // Sampling pass: each thread keeps up to CKR candidate ids of its row in
+  // registers, so testing a token against them touches no memory (a global
+  // load there waits for every copy in flight, and so does an LDS read, which
+  // the compiler cannot tell apart from the copies' destinations).
+  static constexpr int CKR = BR <= 64 ? 16 : 8;
   // survivors a position's queue holds per tile (the queues use the stage
   // buffer the epilogue aliases)
   static constexpr int QCAP = STAGE_BYTES / (BR * 8);
@@ -157,6 +162,17 @@ __device__ __forceinline__ bool is_candidate(const SampleArgs& sa, uint64_t mask
 #pragma unroll
     for (int q = 0; q < 8; ++q) hit |= (k0 + q < sa.K) & (clamp_id(t[q], V) == v);
   }
+  return hit != 0;
+}
+
+// The same test against the row's ids held in registers (already clamped;
+// unused slots hold -1).
+template <int N>
+__device__ __forceinline__ bool is_candidate_reg(const int (&ids)[N], uint64_t mask, int v) {
+  if (!((mask >> (v & 63)) & 1ull)) return false;
+  int hit = 0;
+#pragma unroll
+  for (int k = 0; k < N; ++k) hit |= ids[k] == v;
   return hit != 0;
 }
 
@@ -264,8 +280,20 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   constexpr int kColUnroll = SAMPLE ? (C::BR >= 128 ? 1 : kColTwo) : (KP >= 64 ? kColTwo : kColFull);
   const bool row_ok = r0 + ep < rows;
   uint64_t cmask = 0;
+  constexpr int kCandRegs = SAMPLE ? C::CKR : 1;
+  int cid_reg[kCandRegs];
+#pragma unroll
+  for (int k = 0; k < kCandRegs; ++k) cid_reg[k] = -1;
+  const bool cand_reg = SAMPLE && sa.K <= C::CKR;
   if constexpr (SAMPLE) {
-    if (row_ok) cmask = candidate_mask(sa, r0 + ep, V);
+    if (row_ok) {
+      cmask = candidate_mask(sa, r0 + ep, V);
+      if (cand_reg) {
+#pragma unroll
+        for (int k = 0; k < kCandRegs; ++k)
+          if (k < sa.K) cid_reg[k] = clamp_id(sa.cand_id[static_cast<size_t>(r0 + ep) * sa.K + k], V);
+      }
+    }
   }
 
   // One float4 of staged logits (columns col..col+3 of chunk x) of this
@@ -305,7 +333,9 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         if (vid < vend && v[q] >= thr && key > list[KP - 1]) {
           // sampling keeps candidates out: their draws use exact weights
           if constexpr (SAMPLE) {
-            if (!row_ok || is_candidate(sa, cmask, r0 + ep, vid, V)) continue;
+            if (!row_ok) continue;
+            if (cand_reg ? is_candidate_reg(cid_reg, cmask, vid) : is_candidate(sa, cmask, r0 + ep, vid, V))
+              continue;
           }
           list_insert(list, key);
         }
