@@ -135,9 +135,14 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
       const int n = n0 + wn * 32 + y * 16 + (lane & 15);
       const int jb0 = j0 + wj * 32 + x * 16 + (lane >> 4) * 4;
       if (n < jb.n) {
+        float* o = out + static_cast<size_t>(n) * jb.J + jb0;
+        if (jb0 + 4 <= jb.J && (reinterpret_cast<uintptr_t>(o) & 15u) == 0) {
+          *reinterpret_cast<float4*>(o) = make_float4(acc[x][y][0], acc[x][y][1], acc[x][y][2], acc[x][y][3]);
+        } else {
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          if (jb0 + q < jb.J) out[static_cast<size_t>(n) * jb.J + jb0 + q] = acc[x][y][q];
+          for (int q = 0; q < 4; ++q)
+            if (jb0 + q < jb.J) o[q] = acc[x][y][q];
+        }
       }
     }
 }
@@ -381,6 +386,11 @@ __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
     const int n = n0 + b * 16 + (lane & 15);
     if (n >= jb.n) continue;
     float* o = out_row(n);
+    if (jq + 4 <= ds && (reinterpret_cast<uintptr_t>(o + jq) & 15u) == 0) {
+      // four consecutive outputs of the row in one 16-byte store
+      *reinterpret_cast<float4*>(o + jq) = make_float4(acc[b][0], acc[b][1], acc[b][2], acc[b][3]);
+      continue;
+    }
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int j = jq + q;
