@@ -2,8 +2,8 @@
 """Benchmark of one BRISK-DLM decoding step on one MI355X.
 
 A step is the whole hot path over one block batch: brisk_propose_block (LM
-head + fused top-K), brisk_rerank (the prefix-conditioned corrector) and
-brisk_verify_accept (greedy verification).  Inputs are synthetic, drawn once
+head + fused top-K) and brisk_rerank_verify (the prefix-conditioned corrector
+followed by greedy verification of its selections).  Inputs are synthetic, drawn once
 on the GPU and resident in HBM before timing starts.
 
 Prints one JSON line: block positions per second, the propose stage's
@@ -288,9 +288,8 @@ def main():
         merge()
 
     def rest():
-        brisk.rerank(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, wl.B, wl.L, selected=sel,
-                     workspace=ws_r)
-        brisk.verify_accept(sel, blk.verifier, accept_len=acc, correction=cor)
+        brisk.rerank_verify(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, blk.verifier, wl.B, wl.L,
+                            selected=sel, accept_len=acc, correction=cor, workspace=ws_r)
 
     for _ in range(args.warmup):
         propose()

@@ -183,6 +183,26 @@ int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_
 int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,
                         int32_t* accept_len, int32_t* correction, void* stream);
 
+/*
+ * brisk_rerank followed by brisk_verify_accept on its selections, in one call
+ * (Algorithm 1(b): select, then verify).  Same arguments as brisk_rerank plus
+ *
+ *   verifier    [B, L] int32  the verifier's token at every position
+ *   accept_len  [B] int32 out, correction [B] int32 out (nullable), as in
+ *               brisk_verify_accept
+ *
+ * When the single-wavefront scan runs (d_state <= 256, K <= 16) the scan
+ * itself compares each selection with the verifier's token, so no separate
+ * launch follows; otherwise the verification kernel runs after the scan.
+ * Results equal the two calls made one after the other.
+ */
+int brisk_rerank_verify(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                        const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                        const float* cand_logit, const int32_t* cand_id, const int32_t* verifier,
+                        int32_t B, int32_t L, int32_t K, int32_t d, int32_t V, int32_t* selected,
+                        float* refined, float* gamma, float* resid, int32_t* accept_len,
+                        int32_t* correction, void* ws, size_t ws_bytes, void* stream);
+
 /* Workspace bytes brisk_propose_verify needs (written to *bytes). */
 int brisk_propose_verify_workspace_size(int32_t rows_prop, int32_t rows_ver, int32_t d, int32_t V,
                                         int32_t K, size_t* bytes);

@@ -11,6 +11,7 @@ Entry points (same names as the C ABI):
 * :func:`propose_block` - LM-head logits and ordered top-K candidates;
 * :func:`rerank` - the prefix-conditioned corrector over the candidates;
 * :func:`verify_accept` - greedy verification: accept length and correction;
+* :func:`rerank_verify` - :func:`rerank` and :func:`verify_accept` in one call;
 * :func:`propose_verify` - one LM-head pass for proposal rows (top-K) and
   verifier rows (argmax);
 * :func:`verify_commit` - greedy verification and the committed tokens;
@@ -28,14 +29,14 @@ from typing import Dict, Optional, Tuple
 
 import torch
 
-__all__ = ["BriskError", "Corrector", "propose_block", "propose_lmhead", "propose_merge", "rerank", "verify_accept", "accept_profile",
+__all__ = ["BriskError", "Corrector", "propose_block", "propose_lmhead", "propose_merge", "rerank", "rerank_verify", "verify_accept", "accept_profile",
            "propose_verify", "verify_commit", "corrector_loss", "spec_verify",
            "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
 ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
                "brisk_propose_block", "brisk_propose_lmhead", "brisk_propose_merge",
-               "brisk_rerank_workspace_size", "brisk_rerank",
+               "brisk_rerank_workspace_size", "brisk_rerank", "brisk_rerank_verify",
                "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
                "brisk_verify_commit", "brisk_spec_verify_workspace_size", "brisk_spec_verify",
                "brisk_corrector_loss", "brisk_accept_profile_workspace_size",
@@ -92,6 +93,10 @@ def lib() -> ctypes.CDLL:
             L.brisk_rerank.restype = ctypes.c_int
             L.brisk_rerank.argtypes = [ctypes.POINTER(_CorrectorC), _p, _p, _p, _p, _p, _p, _p,
                                        _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _sz, _p]
+            L.brisk_rerank_verify.restype = ctypes.c_int
+            L.brisk_rerank_verify.argtypes = [ctypes.POINTER(_CorrectorC), _p, _p, _p, _p, _p, _p, _p, _p,
+                                              _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p,
+                                              _p, _sz, _p]
             L.brisk_verify_accept.restype = ctypes.c_int
             L.brisk_verify_accept.argtypes = [_p, _p, _i32, _i32, _p, _p, _p]
             L.brisk_propose_verify_workspace_size.restype = ctypes.c_int
@@ -260,14 +265,8 @@ def rerank_workspace_size(corr: Corrector, B: int, L: int, K: int) -> int:
     return out.value
 
 
-def rerank(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anchor_tok: torch.Tensor,
-           lm_head: torch.Tensor, tok_embed: torch.Tensor, cand_logit: torch.Tensor,
-           cand_id: torch.Tensor, B: int, L: int, *, want_scores: bool = False,
-           selected: Optional[torch.Tensor] = None, refined: Optional[torch.Tensor] = None,
-           gamma: Optional[torch.Tensor] = None, resid: Optional[torch.Tensor] = None,
-           workspace: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
-    """Run the corrector; returns {"selected": [B,L] int32} plus "refined", "gamma",
-    "resid" when ``want_scores`` (or when the caller passes those buffers)."""
+def _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id, B, L,
+                 want_scores, selected, refined, gamma, resid, workspace):
     _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
     _dev_tensor(ctx_hidden, "ctx_hidden", torch.bfloat16, 2)
     _dev_tensor(anchor_tok, "anchor_tok", torch.int32, 1)
@@ -293,16 +292,62 @@ def rerank(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anch
             resid = torch.empty(rows, K, dtype=torch.float32, device=dev)
     need = rerank_workspace_size(corr, B, L, K)
     ws = workspace if workspace is not None else _workspace(dev, need, "rerank")
-    st = lib().brisk_rerank(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
-                            _ptr(anchor_tok), _ptr(lm_head), _ptr(tok_embed), _ptr(cand_logit),
-                            _ptr(cand_id), B, L, K, d, V, _ptr(selected), _ptr(refined), _ptr(gamma),
-                            _ptr(resid), _ptr(ws), ws.numel() * ws.element_size(),
-                            _stream_ptr(dev, stream))
-    _check(st, "brisk_rerank")
     out = {"selected": selected}
     for k, v in (("refined", refined), ("gamma", gamma), ("resid", resid)):
         if v is not None:
             out[k] = v
+    return K, d, V, dev, ws, out
+
+
+def rerank(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anchor_tok: torch.Tensor,
+           lm_head: torch.Tensor, tok_embed: torch.Tensor, cand_logit: torch.Tensor,
+           cand_id: torch.Tensor, B: int, L: int, *, want_scores: bool = False,
+           selected: Optional[torch.Tensor] = None, refined: Optional[torch.Tensor] = None,
+           gamma: Optional[torch.Tensor] = None, resid: Optional[torch.Tensor] = None,
+           workspace: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
+    """Run the corrector; returns {"selected": [B,L] int32} plus "refined", "gamma",
+    "resid" when ``want_scores`` (or when the caller passes those buffers)."""
+    K, d, V, dev, ws, out = _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                                         cand_logit, cand_id, B, L, want_scores, selected, refined,
+                                         gamma, resid, workspace)
+    st = lib().brisk_rerank(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
+                            _ptr(anchor_tok), _ptr(lm_head), _ptr(tok_embed), _ptr(cand_logit),
+                            _ptr(cand_id), B, L, K, d, V, _ptr(out["selected"]), _ptr(out.get("refined")),
+                            _ptr(out.get("gamma")), _ptr(out.get("resid")), _ptr(ws),
+                            ws.numel() * ws.element_size(), _stream_ptr(dev, stream))
+    _check(st, "brisk_rerank")
+    return out
+
+
+def rerank_verify(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anchor_tok: torch.Tensor,
+                  lm_head: torch.Tensor, tok_embed: torch.Tensor, cand_logit: torch.Tensor,
+                  cand_id: torch.Tensor, verifier: torch.Tensor, B: int, L: int, *,
+                  want_scores: bool = False, selected: Optional[torch.Tensor] = None,
+                  refined: Optional[torch.Tensor] = None, gamma: Optional[torch.Tensor] = None,
+                  resid: Optional[torch.Tensor] = None, accept_len: Optional[torch.Tensor] = None,
+                  correction: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                  stream=None) -> Dict[str, torch.Tensor]:
+    """:func:`rerank` then :func:`verify_accept` on its selections, in one call.
+    Returns the rerank outputs plus "accept_len" and "correction" [B] int32."""
+    _dev_tensor(verifier, "verifier", torch.int32, 2)
+    if tuple(verifier.shape) != (B, L):
+        raise ValueError("verifier must be [B, L]")
+    K, d, V, dev, ws, out = _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                                         cand_logit, cand_id, B, L, want_scores, selected, refined,
+                                         gamma, resid, workspace)
+    if accept_len is None:
+        accept_len = torch.empty(B, dtype=torch.int32, device=dev)
+    if correction is None:
+        correction = torch.empty(B, dtype=torch.int32, device=dev)
+    st = lib().brisk_rerank_verify(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
+                                   _ptr(anchor_tok), _ptr(lm_head), _ptr(tok_embed), _ptr(cand_logit),
+                                   _ptr(cand_id), _ptr(verifier), B, L, K, d, V, _ptr(out["selected"]),
+                                   _ptr(out.get("refined")), _ptr(out.get("gamma")), _ptr(out.get("resid")),
+                                   _ptr(accept_len), _ptr(correction), _ptr(ws),
+                                   ws.numel() * ws.element_size(), _stream_ptr(dev, stream))
+    _check(st, "brisk_rerank_verify")
+    out["accept_len"] = accept_len
+    out["correction"] = correction
     return out
 
 

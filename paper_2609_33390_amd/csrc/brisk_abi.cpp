@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 6;
+constexpr int kAbiVersion = 7;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 
@@ -177,11 +177,14 @@ int brisk_rerank_workspace_size(const brisk_corrector* c, int32_t B, int32_t L, 
   return BRISK_OK;
 }
 
-int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
-                 const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
-                 const float* cand_logit, const int32_t* cand_id, int32_t B, int32_t L, int32_t K,
-                 int32_t d, int32_t V, int32_t* selected, float* refined, float* gamma,
-                 float* resid, void* ws, size_t ws_bytes, void* stream) {
+namespace {
+
+int rerank_impl(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                const float* cand_logit, const int32_t* cand_id, const int32_t* verifier, int32_t B,
+                int32_t L, int32_t K, int32_t d, int32_t V, int32_t* selected, float* refined,
+                float* gamma, float* resid, int32_t* accept_len, int32_t* correction, void* ws,
+                size_t ws_bytes, void* stream) {
   int st = corrector_check(c);
   if (st != BRISK_OK) return st;
   if (!hidden || !ctx_hidden || !anchor_tok || !lm_head || !tok_embed || !cand_logit ||
@@ -202,9 +205,34 @@ int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_
   if (ws_bytes < need || !ws) return BRISK_ERR_WORKSPACE;
   if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
   brisk::launch_rerank(*c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
-                       B, L, K, d, V, selected, refined, gamma, resid, ws,
-                       static_cast<hipStream_t>(stream));
+                       B, L, K, d, V, selected, refined, gamma, resid, verifier, accept_len,
+                       correction, ws, static_cast<hipStream_t>(stream));
   return launch_status();
+}
+
+}  // namespace
+
+int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                 const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                 const float* cand_logit, const int32_t* cand_id, int32_t B, int32_t L, int32_t K,
+                 int32_t d, int32_t V, int32_t* selected, float* refined, float* gamma,
+                 float* resid, void* ws, size_t ws_bytes, void* stream) {
+  return rerank_impl(c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
+                     nullptr, B, L, K, d, V, selected, refined, gamma, resid, nullptr, nullptr, ws,
+                     ws_bytes, stream);
+}
+
+int brisk_rerank_verify(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                        const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                        const float* cand_logit, const int32_t* cand_id, const int32_t* verifier,
+                        int32_t B, int32_t L, int32_t K, int32_t d, int32_t V, int32_t* selected,
+                        float* refined, float* gamma, float* resid, int32_t* accept_len,
+                        int32_t* correction, void* ws, size_t ws_bytes, void* stream) {
+  if (!verifier || !accept_len) return BRISK_ERR_NULL;
+  if (!aligned4(verifier) || !aligned4(accept_len) || !aligned4(correction)) return BRISK_ERR_UNSUPPORTED;
+  return rerank_impl(c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
+                     verifier, B, L, K, d, V, selected, refined, gamma, resid, accept_len, correction,
+                     ws, ws_bytes, stream);
 }
 
 int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,

@@ -473,6 +473,11 @@ struct ScanArgs {
   float* gamma;
   float* resid;
   float* dump;       // [B, 64] sink for output lanes with nothing to write
+  // optional verification in the same pass (single-wave scan only): the
+  // verifier's tokens [B, L] and the accepted-prefix length / correction [B]
+  const int32_t* verifier;
+  int32_t* accept_len;
+  int32_t* correction;
 };
 
 template <int KM>
@@ -804,6 +809,16 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
   // K..2K-1 the residuals, lane 62 the gate, lane 63 the selected id; lanes
   // without an output (or whose output was not requested) write to a sink.
   const bool want = a.refined != nullptr || a.resid != nullptr;
+  // Verification on the fly: step i's selection sits in lane i % 64; at the
+  // end of every 64 steps a ballot against the verifier's tokens of those
+  // steps (loaded a chunk ahead) finds the first mismatch.
+  const bool fuse = a.verifier != nullptr;
+  int mysel = 0, first_mis = L, corr_tok = -1;
+  auto load_ver = [&](int c0) {
+    const int i = c0 + lane;
+    return fuse && i < L ? a.verifier[row0 + i] : 0;
+  };
+  int vchunk = load_ver(0);
   const int kd = lane < K ? lane : lane - K;
   float* obase = a.dump + static_cast<size_t>(b) * 64 + lane;
   size_t ostride = 0;
@@ -901,6 +916,22 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
     }
     ov = lane == 63 ? __int_as_float(sel) : ov;
     obase[(row0 + i) * ostride] = ov;
+    if (fuse) {
+      mysel = lane == (i & 63) ? sel : mysel;
+      if ((i & 63) == 63 || i == L - 1) {
+        const int c0 = i & ~63;
+        const uint64_t mis = __ballot(c0 + lane <= i && mysel != vchunk);
+        if (first_mis == L && mis) {
+          first_mis = c0 + static_cast<int>(__builtin_ctzll(mis));
+          corr_tok = __builtin_amdgcn_readlane(vchunk, first_mis - c0);
+        }
+        if (i + 1 < L) vchunk = load_ver(c0 + 64);
+      }
+    }
+  }
+  if (fuse && lane == 0) {
+    a.accept_len[b] = first_mis;
+    if (a.correction) a.correction[b] = first_mis < L ? corr_tok : -1;
   }
 }
 
@@ -972,7 +1003,8 @@ size_t rerank_workspace_bytes(const brisk_corrector& c, int B, int L, int K) {
 void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint16_t* ctx_hidden,
                    const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
                    const float* cand_logit, const int32_t* cand_id, int B, int L, int K, int d,
-                   int V, int32_t* selected, float* refined, float* gamma, float* resid, void* ws,
+                   int V, int32_t* selected, float* refined, float* gamma, float* resid,
+                   const int32_t* verifier, int32_t* accept_len, int32_t* correction, void* ws,
                    hipStream_t s) {
   const Layout lay = rerank_layout(c, B, L, K);
   char* base = static_cast<char*>(ws);
@@ -1061,6 +1093,12 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   sa.cand_logit = cand_logit; sa.cand_id = cand_id; sa.anchor = anchor_tok;
   sa.selected = selected; sa.refined = refined; sa.gamma = gamma; sa.resid = resid;
   sa.dump = F(lay.DUMP);
+  const bool pc = ds <= 256 && K <= 16;  // the single-wave scan, which can verify in the same pass
+  if (verifier && pc) {
+    sa.verifier = verifier;
+    sa.accept_len = accept_len;
+    sa.correction = correction;
+  }
   const int nw = (ds + 63) / 64;
   if (ds <= 256 && K <= 8)
     hipLaunchKernelGGL((scan_pc_kernel<8, 4>), dim3(B), dim3(128), 0, s, sa);
@@ -1069,6 +1107,7 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   else if (K <= 8) launch_scan<8, 4>(sa, B, nw, s);
   else if (K <= 16) launch_scan<16, 3>(sa, B, nw, s);
   else launch_scan<64, 1>(sa, B, nw, s);
+  if (verifier && !pc) launch_verify(selected, verifier, B, L, accept_len, correction, s);
 }
 
 }  // namespace brisk

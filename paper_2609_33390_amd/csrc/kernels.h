@@ -36,7 +36,8 @@ size_t rerank_workspace_bytes(const brisk_corrector& c, int B, int L, int K);
 void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint16_t* ctx_hidden,
                    const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
                    const float* cand_logit, const int32_t* cand_id, int B, int L, int K, int d,
-                   int V, int32_t* selected, float* refined, float* gamma, float* resid, void* ws,
+                   int V, int32_t* selected, float* refined, float* gamma, float* resid,
+                   const int32_t* verifier, int32_t* accept_len, int32_t* correction, void* ws,
                    hipStream_t s);
 
 // ---- verify -----------------------------------------------------------------

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 6
+    assert L.brisk_abi_version() == 7
     for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5):
         assert L.brisk_status_str(st).decode()
     assert L.brisk_status_str(123).decode() == "unknown status"
@@ -128,6 +128,28 @@ def _rerank(c=None, **kw):
 ])
 def test_rerank_validation(ckw, kw, want):
     assert _rerank(_corr(**ckw), **kw) == want
+
+
+def _rerank_verify(c=None, **kw):
+    a = dict(hidden=FAKE, ctx=FAKE, anchor=FAKE, W=FAKE, E=FAKE, cl=FAKE, ci=FAKE, ver=FAKE, B=1, L=32, K=8,
+             d=4096, V=126464, sel=FAKE, ref=None, gam=None, res=None, acc=FAKE, cor=None, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    c = _corr() if c is None else c
+    return brisk.lib().brisk_rerank_verify(ctypes.byref(c), a["hidden"], a["ctx"], a["anchor"], a["W"], a["E"],
+                                           a["cl"], a["ci"], a["ver"], a["B"], a["L"], a["K"], a["d"], a["V"],
+                                           a["sel"], a["ref"], a["gam"], a["res"], a["acc"], a["cor"], a["ws"],
+                                           a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("ckw,kw,want", [
+    ({}, dict(ver=None), ENULL), ({}, dict(acc=None), ENULL), ({}, dict(sel=None), ENULL),
+    (dict(W_z=None), {}, ENULL),
+    ({}, dict(ver=MISALIGNED), EUNSUP), ({}, dict(acc=MISALIGNED), EUNSUP), ({}, dict(cor=MISALIGNED), EUNSUP),
+    ({}, dict(K=65), ESHAPE), ({}, dict(L=33), ESHAPE), (dict(d_state=513), {}, ESHAPE),
+    ({}, dict(ws_bytes=16), EWS), ({}, dict(cor=FAKE, ws_bytes=16), EWS),
+])
+def test_rerank_verify_validation(ckw, kw, want):
+    assert _rerank_verify(_corr(**ckw), **kw) == want
 
 
 def test_rerank_workspace_size_query():

@@ -76,6 +76,15 @@ def test_step_entry_points_stay_in_bounds(name, B, L, d, V, K):
     brisk.verify_accept(sel.t, blk.verifier, accept_len=acc.t, correction=cor.t)
     _check(acc, cor)
 
+    sel2, gam2 = Guarded((B, L), torch.int32), Guarded((rows,), torch.float32)
+    ref2, res2 = Guarded((rows, K), torch.float32), Guarded((rows, K), torch.float32)
+    acc3, cor3, wsr2 = Guarded((B,), torch.int32), Guarded((B,), torch.int32), _ws(wsr.nbytes)
+    brisk.rerank_verify(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl.t, ci.t, blk.verifier, B, L,
+                        selected=sel2.t, refined=ref2.t, gamma=gam2.t, resid=res2.t, accept_len=acc3.t,
+                        correction=cor3.t, workspace=wsr2.t)
+    _check(sel2, ref2, res2, gam2, acc3, cor3, wsr2)
+    assert torch.equal(acc3.t, acc.t) and torch.equal(cor3.t, cor.t)
+
     L_ = brisk.lib()
     acc2, com, ncom = Guarded((B,), torch.int32), Guarded((B, L + 1), torch.int32), Guarded((B,), torch.int32)
     st = L_.brisk_verify_commit(sel.t.data_ptr(), blk.verifier.data_ptr(), B, L, acc2.t.data_ptr(),

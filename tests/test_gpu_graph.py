@@ -1,6 +1,7 @@
 """GPU checks of the launch structure: the LM-head pass and the merge called
 separately equal brisk_propose_block, and a hipGraph capture of the whole step
-(propose, rerank, verify) reproduces the eager results on every replay."""
+(propose, rerank, verify; the last two also as the single rerank_verify call)
+reproduces the eager results on every replay."""
 import pytest
 import torch
 
@@ -26,8 +27,9 @@ def test_split_launches_equal_the_composed_call(name):
     assert torch.equal(cl, cl2) and torch.equal(ci, ci2)
 
 
+@pytest.mark.parametrize("fused", [False, True])
 @pytest.mark.parametrize("name", ["tiny-d64-v512", "llada8b-b1-l32"])
-def test_graph_replay_matches_eager(name):
+def test_graph_replay_matches_eager(name, fused):
     wl = synth.WORKLOADS[name]
     blk = synth.make_block(wl, "cuda")
     corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
@@ -44,6 +46,10 @@ def test_graph_replay_matches_eager(name):
     def step():
         brisk.propose_lmhead(blk.H, blk.W, K, ws_p)
         brisk.propose_merge(rows, wl.V, K, ws_p, cl, ci)
+        if fused:
+            brisk.rerank_verify(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, blk.verifier, wl.B, wl.L,
+                                selected=sel, accept_len=acc, correction=cor, workspace=ws_r)
+            return
         brisk.rerank(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, wl.B, wl.L, selected=sel,
                      workspace=ws_r)
         brisk.verify_accept(sel, blk.verifier, accept_len=acc, correction=cor)
