@@ -9,9 +9,12 @@
 // a per-previous-token part and a 5-wide feature part; the residual
 // <W_s u_i, W_c E_out(v)> re-associates to <u_i, W_s^T W_c E_out(v)>.  All of
 // those pieces are computed up front for every row and every candidate
-// (kernels gather_proj, cross_dot and lift); the scan then carries only
+// (kernels gather_proj, which also forms the cross logits, and lift); the
+// scan then carries only
 // the selection-dependent chain: features, gate, state update, K dot products
 // and an argmax per step, one wavefront per sequence.
+#include <algorithm>
+
 #include "device_common.h"
 #include "kernels.h"
 
@@ -36,16 +39,78 @@ struct ProjJob {
   size_t slice_stride;  // floats between consecutive slices
 };
 constexpr int kMaxProjJobs = 6;
+// The cross logits ride in the same launch as one more job row: dot product n
+// < NC is candidate k of row r against hidden row r+1 (0 on the last row of a
+// block); n >= NC is the anchor token x_0 against the block's first row.
+struct CrossJob {
+  const uint16_t* W;
+  const uint16_t* H;
+  const int32_t* cand_id;
+  const int32_t* anchor;
+  int B, L, K, V;
+  float* X;
+};
 struct ProjJobs {
   ProjJob job[kMaxProjJobs];
+  CrossJob cross;
   int d, splits;
 };
 
 constexpr int PJ_BN = 64, PJ_BJ = 64, PJ_BK = 64, PJ_STRIDE = PJ_BK + 8;
+constexpr int PJ_PF = 2;  // reduction chunks in flight per thread
+
+// One wavefront per cross logit, eight 16-byte loads of each operand in
+// flight per lane.
+__device__ void cross_dots(const CrossJob& cj, int d) {
+  const int lane = threadIdx.x & 63;
+  const int NC = cj.B * cj.L * cj.K;
+  const int waves = gridDim.x * gridDim.z * 4;
+  for (int n = (blockIdx.z * gridDim.x + blockIdx.x) * 4 + (threadIdx.x >> 6); n < NC + cj.B; n += waves) {
+    int v, hrow;
+    if (n < NC) {
+      const int r = n / cj.K;
+      if (r % cj.L == cj.L - 1) {
+        if (lane == 0) cj.X[n] = 0.f;
+        continue;
+      }
+      v = clamp_id(cj.cand_id[n], cj.V);
+      hrow = r + 1;
+    } else {
+      const int b = n - NC;
+      v = clamp_id(cj.anchor[b], cj.V);
+      hrow = b * cj.L;
+    }
+    const uint16_t* w = cj.W + static_cast<size_t>(v) * d;
+    const uint16_t* h = cj.H + static_cast<size_t>(hrow) * d;
+    float s = 0.f;
+    for (int k0 = lane * 8; k0 < d; k0 += 8 * 512) {
+      uint4 a[8], c[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int k = k0 + u * 512;
+        a[u] = k < d ? *reinterpret_cast<const uint4*>(w + k) : make_uint4(0, 0, 0, 0);
+        c[u] = k < d ? *reinterpret_cast<const uint4*>(h + k) : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        s += bf16_lo(a[u].x) * bf16_lo(c[u].x) + bf16_hi(a[u].x) * bf16_hi(c[u].x);
+        s += bf16_lo(a[u].y) * bf16_lo(c[u].y) + bf16_hi(a[u].y) * bf16_hi(c[u].y);
+        s += bf16_lo(a[u].z) * bf16_lo(c[u].z) + bf16_hi(a[u].z) * bf16_hi(c[u].z);
+        s += bf16_lo(a[u].w) * bf16_lo(c[u].w) + bf16_hi(a[u].w) * bf16_hi(c[u].w);
+      }
+    }
+    s = wave_sum(s);
+    if (lane == 0) cj.X[n] = s;
+  }
+}
 
 __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
-  const ProjJob& jb = jobs.job[blockIdx.y];
   const int d = jobs.d;
+  if (blockIdx.y == kMaxProjJobs) {
+    cross_dots(jobs.cross, d);
+    return;
+  }
+  const ProjJob& jb = jobs.job[blockIdx.y];
   const int n_jt = (jb.J + PJ_BJ - 1) / PJ_BJ;
   const int n_nt = (jb.n + PJ_BN - 1) / PJ_BN;
   if (static_cast<int>(blockIdx.x) >= n_jt * n_nt) return;
@@ -54,7 +119,7 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   const int chunks = (d + PJ_BK - 1) / PJ_BK;
   const int per = (chunks + jobs.splits - 1) / jobs.splits;
   const int c_begin = min(static_cast<int>(blockIdx.z) * per, chunks);
-  const int c_end = min(c_begin + per, chunks);
+  const int n_ch = min(c_begin + per, chunks) - c_begin;
 
   __shared__ __align__(16) uint16_t sA[PJ_BJ * PJ_STRIDE];
   __shared__ __align__(16) uint16_t sB[PJ_BN * PJ_STRIDE];
@@ -62,35 +127,45 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wj = wave & 1, wn = wave >> 1;  // 2 x 2 waves, 32 x 32 each
 
-  // Each thread stages two 16-byte chunks of each operand per step; its
-  // rows are fixed, so the gathered table rows are resolved once.
+  // Each thread stages two 16-byte pieces of each operand per chunk; its
+  // rows are fixed, so the gathered table rows are resolved once.  PJ_PF
+  // chunks are in flight in registers, so a workgroup with a short slice of
+  // the reduction waits about one memory latency, not one per chunk.  Every
+  // load is unconditional and reads valid memory, so the compiler counts the
+  // loads in flight exactly and waits only for the chunk being staged: rows
+  // past J or n read a valid row whose outputs are never stored, and pieces
+  // past d or past the slice (the tail of the last group re-reads the slice's
+  // last chunk) are staged as zeros.
   int arow[2], brow[2], col[2];
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const int c = tid + i * 256;
     const int row = c >> 3;
     col[i] = (c & 7) * 8;
-    arow[i] = j0 + row < jb.J ? j0 + row : -1;
+    arow[i] = j0 + row < jb.J ? j0 + row : 0;
     const int n = n0 + row;
-    brow[i] = n < jb.n ? (jb.idx ? clamp_id(jb.idx[n], jb.n_table) : n) : -1;
+    brow[i] = n < jb.n ? (jb.idx ? clamp_id(jb.idx[n], jb.n_table) : n) : 0;
   }
-  uint4 ra[2], rb[2];
-  auto load = [&](int k0) {
+  uint4 ra[PJ_PF][2], rb[PJ_PF][2];
+  auto load = [&](uint4 (&A)[2], uint4 (&Bv)[2], int ch) {
+    const int cc = c_begin + max(min(ch, n_ch - 1), 0);
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int k = k0 + col[i];
-      ra[i] = make_uint4(0, 0, 0, 0);
-      rb[i] = make_uint4(0, 0, 0, 0);
-      if (arow[i] >= 0 && k < d) ra[i] = *reinterpret_cast<const uint4*>(jb.wt + static_cast<size_t>(arow[i]) * d + k);
-      if (brow[i] >= 0 && k < d) rb[i] = *reinterpret_cast<const uint4*>(jb.table + static_cast<size_t>(brow[i]) * d + k);
+      const int k = cc * PJ_BK + col[i];
+      const int kc = k < d ? k : 0;
+      A[i] = *reinterpret_cast<const uint4*>(jb.wt + static_cast<size_t>(arow[i]) * d + kc);
+      Bv[i] = *reinterpret_cast<const uint4*>(jb.table + static_cast<size_t>(brow[i]) * d + kc);
     }
   };
-  auto store = [&]() {
+  auto store = [&](const uint4 (&A)[2], const uint4 (&Bv)[2], int ch) {
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int row = (tid + i * 256) >> 3;
-      *reinterpret_cast<uint4*>(sA + row * PJ_STRIDE + col[i]) = ra[i];
-      *reinterpret_cast<uint4*>(sB + row * PJ_STRIDE + col[i]) = rb[i];
+      const uint32_t m = ch < n_ch && (c_begin + ch) * PJ_BK + col[i] < d ? ~0u : 0u;
+      *reinterpret_cast<uint4*>(sA + row * PJ_STRIDE + col[i]) =
+          make_uint4(A[i].x & m, A[i].y & m, A[i].z & m, A[i].w & m);
+      *reinterpret_cast<uint4*>(sB + row * PJ_STRIDE + col[i]) =
+          make_uint4(Bv[i].x & m, Bv[i].y & m, Bv[i].z & m, Bv[i].w & m);
     }
   };
 
@@ -100,13 +175,22 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-  if (c_begin < c_end) {
-    load(c_begin * PJ_BK);
-    store();
-    __syncthreads();
-    for (int ch = c_begin; ch < c_end; ++ch) {
-      const bool more = ch + 1 < c_end;
-      if (more) load((ch + 1) * PJ_BK);
+  // the scheduling barriers keep the loads in chunk order, which is what
+  // lets each staging step wait for its own chunk only
+#pragma unroll
+  for (int p = 0; p < PJ_PF; ++p) {
+    load(ra[p], rb[p], p);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  for (int g = 0; g < n_ch; g += PJ_PF) {
+#pragma unroll
+    for (int p = 0; p < PJ_PF; ++p) {
+      const int ch = g + p;
+      store(ra[p], rb[p], ch);
+      __syncthreads();
+      __builtin_amdgcn_sched_barrier(0);
+      load(ra[p], rb[p], ch + PJ_PF);
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int kk = 0; kk < PJ_BK; kk += 32) {
         const int koff = kk + (lane >> 4) * 8;
@@ -122,8 +206,6 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
           for (int y = 0; y < 2; ++y)
             acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
       }
-      __syncthreads();
-      if (more) store();
       __syncthreads();
     }
   }
@@ -145,51 +227,6 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
         }
       }
     }
-}
-
-// ---------------------------------------------------------------------------
-// cross_dot: the full-vocabulary logit of every possible previous token at the
-// next position.  n < NC: candidate k of row r against hidden row r+1 (0 on
-// the last row of a block); n >= NC: anchor token x_0 against the block's
-// first row.  One wavefront per dot product.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void cross_dot_kernel(const uint16_t* __restrict__ W,
-                                                        const uint16_t* __restrict__ H,
-                                                        const int32_t* __restrict__ cand_id,
-                                                        const int32_t* __restrict__ anchor, int B,
-                                                        int L, int K, int d, int V,
-                                                        float* __restrict__ X) {
-  const int lane = threadIdx.x & 63;
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int NC = B * L * K;
-  if (n >= NC + B) return;
-  int v, hrow;
-  if (n < NC) {
-    const int r = n / K;
-    if (r % L == L - 1) {
-      if (lane == 0) X[n] = 0.f;
-      return;
-    }
-    v = clamp_id(cand_id[n], V);
-    hrow = r + 1;
-  } else {
-    const int b = n - NC;
-    v = clamp_id(anchor[b], V);
-    hrow = b * L;
-  }
-  const uint16_t* w = W + static_cast<size_t>(v) * d;
-  const uint16_t* h = H + static_cast<size_t>(hrow) * d;
-  float s = 0.f;
-  for (int k = lane * 8; k < d; k += 64 * 8) {
-    const uint4 a = *reinterpret_cast<const uint4*>(w + k);
-    const uint4 c = *reinterpret_cast<const uint4*>(h + k);
-    s += bf16_lo(a.x) * bf16_lo(c.x) + bf16_hi(a.x) * bf16_hi(c.x);
-    s += bf16_lo(a.y) * bf16_lo(c.y) + bf16_hi(a.y) * bf16_hi(c.y);
-    s += bf16_lo(a.z) * bf16_lo(c.z) + bf16_hi(a.z) * bf16_hi(c.z);
-    s += bf16_lo(a.w) * bf16_lo(c.w) + bf16_hi(a.w) * bf16_hi(c.w);
-  }
-  s = wave_sum(s);
-  if (lane == 0) X[n] = s;
 }
 
 // ---------------------------------------------------------------------------
@@ -265,62 +302,88 @@ __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
   __shared__ __align__(16) uint16_t s_x[3][2][LT_BN * LT_ROW];
   __shared__ __align__(16) uint16_t s_m[2][LT_BJ * LT_ROW];
 
-  const int CA = jb.t[0].C, c_total = CA + jb.t[1].C;
-  const int nch = (c_total + LT_BC - 1) / LT_BC;
+  // Term 0 fills chunks [0, nc0) and term 1 the rest, so the term of a chunk
+  // is uniform across the workgroup.
+  const int nc0 = (jb.t[0].C + LT_BC - 1) / LT_BC;
+  const int nch = nc0 + (jb.t[1].C + LT_BC - 1) / LT_BC;
   // staging map: 16 consecutive columns of one row per thread
   const int sr = tid >> 2, sc = (tid & 3) * 16;
-  // a matrix stored along j (m_rs == 1) is read along j and transposed
-  const bool mt = jb.t[0].m_rs == 1;
-  float rin[16];
-  uint16_t rm[16];
-  // 16-element runs that stay inside one term and are 16-byte aligned load
-  // as vectors (the host sets vec / mvec when strides and offsets allow it)
+  // Raw words of the thread's input and matrix runs, as loaded.  Every load
+  // is unconditional and reads valid memory (an element outside the term or
+  // the tile reads index 0); masking and unpacking wait until the run is
+  // staged, so a chunk's loads stay in flight across the previous chunk's
+  // products.  Runs that are contiguous and 16-byte aligned (the host sets
+  // vec / mvec) load as vectors.
+  enum { kF32 = 0, kBf16Pairs = 1, kBf16 = 2 };
+  uint32_t rw[16], mw[16];
+  uint32_t in_ok = 0, m_ok = 0;  // bit q: element q of the run is inside its term and tile
+  int in_mode = kF32;
+  bool m_pairs = false, mt = false;
   auto load = [&](int ch) {
+    const bool second = ch >= nc0;
+    const LiftTerm t = second ? jb.t[1] : jb.t[0];
+    const int cbase = (second ? ch - nc0 : ch) * LT_BC;  // first column of the chunk in the term
     const int n = n0 + sr;
-    const int cb = ch * LT_BC + sc;  // first column of this thread's run
-    const LiftTerm& t0 = jb.t[0];
-    if (t0.vec && n < jb.n && cb + 16 <= CA) {
-      const float* p = static_cast<const float*>(t0.in) + static_cast<size_t>(n) * t0.rs + cb;
+    const int nv = n < jb.n ? n : 0;
+    const size_t rbase = static_cast<size_t>(t.period ? nv % t.period : nv) * t.rs;
+    const int c = cbase + sc;
+    if (t.vec) {  // cs == 1 and C % 16 == 0: the run is wholly inside the term or wholly outside
+      const bool ok = n < jb.n && c + 16 <= t.C;
+      in_ok = ok ? 0xFFFFu : 0u;
+      const size_t off = rbase + (ok ? c : 0);
+      if (t.in_bf16) {
+        in_mode = kBf16Pairs;
+        const uint4* p = reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(t.in) + off);
+        const uint4 u0 = p[0], u1 = p[1];
+        rw[0] = u0.x; rw[1] = u0.y; rw[2] = u0.z; rw[3] = u0.w;
+        rw[4] = u1.x; rw[5] = u1.y; rw[6] = u1.z; rw[7] = u1.w;
+      } else {
+        in_mode = kF32;
+        const uint4* p = reinterpret_cast<const uint4*>(static_cast<const float*>(t.in) + off);
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const float4 a = *reinterpret_cast<const float4*>(p + 4 * v);
-        rin[4 * v] = a.x;
-        rin[4 * v + 1] = a.y;
-        rin[4 * v + 2] = a.z;
-        rin[4 * v + 3] = a.w;
+        for (int v = 0; v < 4; ++v) {
+          const uint4 x = p[v];
+          rw[4 * v] = x.x; rw[4 * v + 1] = x.y; rw[4 * v + 2] = x.z; rw[4 * v + 3] = x.w;
+        }
       }
     } else {
+      in_mode = t.in_bf16 ? kBf16 : kF32;
+      in_ok = 0;
+      size_t idx[16];
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        const int c = cb + q;
-        float v = 0.f;
-        if (n < jb.n && c < c_total) v = c < CA ? lift_in(jb.t[0], n, c) : lift_in(jb.t[1], n, c - CA);
-        rin[q] = v;
+        const bool ok = n < jb.n && c + q < t.C;
+        in_ok |= ok ? 1u << q : 0u;
+        idx[q] = ok ? rbase + static_cast<size_t>(c + q) * t.cs : 0;
+      }
+      if (t.in_bf16) {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) rw[q] = static_cast<const uint16_t*>(t.in)[idx[q]];
+      } else {
+#pragma unroll
+        for (int q = 0; q < 16; ++q) rw[q] = static_cast<const uint32_t*>(t.in)[idx[q]];
       }
     }
-    // matrix runs: along c when m_cs == 1, along j when m_rs == 1 (mt)
-    const int j = j0 + (mt ? sc : sr), c = ch * LT_BC + (mt ? sr : sc);
-    const bool run_ok = mt ? (j + 16 <= ds && c < CA) : (j < ds && c + 16 <= CA);
-    if (t0.mvec && run_ok) {
-      const uint16_t* p = t0.m + static_cast<size_t>(j) * t0.m_rs + static_cast<size_t>(c) * t0.m_cs;
-      const uint4 a = *reinterpret_cast<const uint4*>(p), b = *reinterpret_cast<const uint4*>(p + 8);
-      const uint32_t w[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        rm[2 * q] = static_cast<uint16_t>(w[q] & 0xFFFFu);
-        rm[2 * q + 1] = static_cast<uint16_t>(w[q] >> 16);
-      }
+    // matrix run: along c when m_cs == 1, along j when m_rs == 1 (mt)
+    mt = t.m_rs == 1;
+    const int j = j0 + (mt ? sc : sr), cm = cbase + (mt ? sr : sc);
+    m_pairs = t.mvec != 0;
+    if (t.mvec) {
+      const bool ok = mt ? (j + 16 <= ds && cm < t.C) : (j < ds && cm + 16 <= t.C);
+      m_ok = ok ? 0xFFFFu : 0u;
+      const uint4* p = reinterpret_cast<const uint4*>(
+          t.m + (ok ? static_cast<size_t>(j) * t.m_rs + static_cast<size_t>(cm) * t.m_cs : 0));
+      const uint4 u0 = p[0], u1 = p[1];
+      mw[0] = u0.x; mw[1] = u0.y; mw[2] = u0.z; mw[3] = u0.w;
+      mw[4] = u1.x; mw[5] = u1.y; mw[6] = u1.z; mw[7] = u1.w;
     } else {
+      m_ok = 0;
 #pragma unroll
       for (int q = 0; q < 16; ++q) {
-        const int jq = j0 + (mt ? sc + q : sr), cq = ch * LT_BC + (mt ? sr : sc + q);
-        uint16_t v = 0;
-        if (jq < ds && cq < c_total) {
-          const LiftTerm& t = cq < CA ? jb.t[0] : jb.t[1];
-          const int cl = cq < CA ? cq : cq - CA;
-          v = t.m[static_cast<size_t>(jq) * t.m_rs + static_cast<size_t>(cl) * t.m_cs];
-        }
-        rm[q] = v;
+        const int jq = mt ? j + q : j, cq = mt ? cm : cm + q;
+        const bool ok = jq < ds && cq < t.C;
+        m_ok |= ok ? 1u << q : 0u;
+        mw[q] = t.m[ok ? static_cast<size_t>(jq) * t.m_rs + static_cast<size_t>(cq) * t.m_cs : 0];
       }
     }
   };
@@ -329,6 +392,32 @@ __global__ __launch_bounds__(256) void lift_kernel(LiftJobs jobs) {
                       h[4] | (static_cast<uint32_t>(h[5]) << 16), h[6] | (static_cast<uint32_t>(h[7]) << 16));
   };
   auto store = [&](int buf) {
+    // decode (uniform branches), then mask with the per-element bits
+    uint32_t bits[16], h[16];
+    if (in_mode == kBf16Pairs) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) bits[q] = q & 1 ? rw[q >> 1] & 0xFFFF0000u : rw[q >> 1] << 16;
+    } else if (in_mode == kBf16) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) bits[q] = rw[q] << 16;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) bits[q] = rw[q];
+    }
+    if (m_pairs) {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) h[q] = q & 1 ? mw[q >> 1] >> 16 : mw[q >> 1] & 0xFFFFu;
+    } else {
+#pragma unroll
+      for (int q = 0; q < 16; ++q) h[q] = mw[q] & 0xFFFFu;
+    }
+    float rin[16];
+    uint16_t rm[16];
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      rin[q] = __uint_as_float(bits[q] & (0u - ((in_ok >> q) & 1u)));
+      rm[q] = static_cast<uint16_t>(h[q] & (0u - ((m_ok >> q) & 1u)));
+    }
     uint16_t x[3][16];
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
@@ -1032,10 +1121,12 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
     const int t = proj_tiles(pj.job[j].n, pj.job[j].J);
     max_tiles = t > max_tiles ? t : max_tiles;
   }
-  hipLaunchKernelGGL(gather_proj_kernel, dim3(max_tiles, kMaxProjJobs, S), dim3(256), 0, s, pj);
-
-  hipLaunchKernelGGL(cross_dot_kernel, dim3((NP + 3) / 4), dim3(256), 0, s, lm_head, hidden, cand_id,
-                     anchor_tok, B, L, K, d, V, F(lay.X));
+  pj.cross = CrossJob{lm_head, hidden, cand_id, anchor_tok, B, L, K, V, F(lay.X)};
+  // the cross-logit row needs (NP + 3) / 4 workgroups of four wavefronts
+  // (each loops over more when the grid is capped at about 4096 of them)
+  const int cross_x = std::min(((NP + 3) / 4 + S - 1) / S, (4096 + S - 1) / S);
+  const int gx = std::max(max_tiles, cross_x);
+  hipLaunchKernelGGL(gather_proj_kernel, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
 
   if (S > 1) {
     SliceArrs sl{};
@@ -1059,16 +1150,25 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   LiftJobs lj{};
   lj.ds = ds;
   const float* PEa = F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj;
+  // A term's input runs load as vectors when they are contiguous (cs == 1),
+  // whole (C % 16 == 0) and 16-byte aligned; its matrix runs likewise along
+  // c (m_cs == 1, C % 16 == 0) or along j (m_rs == 1, d_state % 16 == 0).
+  auto term = [&](const void* in, int bf16, int rs, int cs, int period, int C, const uint16_t* m,
+                  int m_rs, int m_cs) {
+    const int per16 = bf16 ? 8 : 4;  // elements per 16 bytes
+    const bool a16 = (reinterpret_cast<uintptr_t>(in) & 15u) == 0 && cs == 1 && C % 16 == 0 &&
+                     rs % per16 == 0;
+    const bool m16 = (reinterpret_cast<uintptr_t>(m) & 15u) == 0 &&
+                     (m_cs == 1 ? m_rs % 8 == 0 && C % 16 == 0 : m_rs == 1 && m_cs % 8 == 0 && ds % 16 == 0);
+    return LiftTerm{in, bf16, rs, cs, period, C, m, m_rs, m_cs, a16 ? 1 : 0, m16 ? 1 : 0};
+  };
   // fp32 inputs: the projections, their split-K slices already summed
   auto fterm = [&](const float* in, int C, const uint16_t* m, int m_rs, int m_cs) {
-    const bool a16 = (reinterpret_cast<uintptr_t>(in) & 15u) == 0 && C % 4 == 0;
-    const bool m16 = (reinterpret_cast<uintptr_t>(m) & 15u) == 0 &&
-                     (m_cs == 1 ? m_rs % 8 == 0 : m_rs == 1 && m_cs % 8 == 0);
-    return LiftTerm{in, 0, C, 1, 0, C, m, m_rs, m_cs, a16 ? 1 : 0, m16 ? 1 : 0};
+    return term(in, 0, C, 1, 0, C, m, m_rs, m_cs);
   };
   const LiftTerm none{nullptr, 0, 0, 0, 0, 0, nullptr, 0, 0, 0, 0};
-  const LiftTerm posz{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1, 0, 0};
-  const LiftTerm posh{c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1, 0, 0};
+  const LiftTerm posz = term(c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1);
+  const LiftTerm posh = term(c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1);
   const size_t vds = static_cast<size_t>(ds);
   lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, NC, SB + (2 + K) * vsz, K, blk, vsz};
   lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, NC, SB + (2 + 2 * K) * vsz, K, blk, vsz};
@@ -1078,8 +1178,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, B, F(lay.TZA), 1, vds, vds};
   lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, B, F(lay.THA), 1, vds, vds};
   // feature maps W_z[:, feat] P_phi and W_h[:, feat] P_phi as [5, ds]: input row f is column f of P_phi
-  lj.job[7] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1, 0, 0}, none}, 5, F(lay.FZ), 1, vds, vds};
-  lj.job[8] = LiftJob{{LiftTerm{c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1, 0, 0}, none}, 5, F(lay.FH), 1, vds, vds};
+  lj.job[7] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1), none}, 5, F(lay.FZ), 1, vds, vds};
+  lj.job[8] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1), none}, 5, F(lay.FH), 1, vds, vds};
   const int lift_cols = static_cast<int>(vsz > vds ? vsz : vds);
   const int lift_rows = NC > 2 * B ? NC : 2 * B;
   hipLaunchKernelGGL(lift_kernel, dim3((lift_rows + LT_BN - 1) / LT_BN, (lift_cols + LT_BJ - 1) / LT_BJ, kMaxLiftJobs),
