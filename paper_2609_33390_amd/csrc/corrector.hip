@@ -909,6 +909,27 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
   };
   int vchunk = load_ver(0);
   const int kd = lane < K ? lane : lane - K;
+  // reduce-scatter keep rules and the candidate each lane ends up holding
+  const bool kb0 = lane & 1, kb1 = lane & 2, kb2 = lane & 4, kb3 = lane & 8;
+  const bool kc0 = kb0 != kb2, kc1 = kb1 != kb2;
+  const int my_cand = KM == 16 ? 8 * kc0 + 4 * kc1 + 2 * kb2 + kb3 : 4 * kc0 + 2 * kc1 + kb2;
+  // a lane holding candidate kd (bpermute address)
+  int out_src;
+  {
+    const int o = kd < KM ? kd : 0;
+    int ob0, ob1, ob2, ob3 = 0;
+    if (KM == 16) {
+      ob3 = o & 1;
+      ob2 = (o >> 1) & 1;
+      ob1 = ((o >> 2) & 1) ^ ob2;
+      ob0 = ((o >> 3) & 1) ^ ob2;
+    } else {
+      ob2 = o & 1;
+      ob1 = ((o >> 1) & 1) ^ ob2;
+      ob0 = ((o >> 2) & 1) ^ ob2;
+    }
+    out_src = 4 * (ob0 + 2 * ob1 + 4 * ob2 + 8 * ob3);
+  }
   float* obase = a.dump + static_cast<size_t>(b) * 64 + lane;
   size_t ostride = 0;
   if (lane < K && a.refined) { obase = a.refined + lane; ostride = K; }
@@ -925,7 +946,7 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
     f4_t eh[KM];
 #pragma unroll
     for (int k = 0; k < KM; ++k) eh[k] = sv[64 * (2 + k)];
-    const float cl_l = sc[lane], xs_l = sc[128 + lane];
+    const float cl_l = sc[lane], xs_l = sc[128 + lane], cl_mine = sc[my_cand];
     const int ci_l = __float_as_int(sc[64 + lane]);
     float clu[KM];  // every lane reads the same words: the candidate logits as uniform values
 #pragma unroll
@@ -957,39 +978,58 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
 #pragma unroll
     for (int k = 0; k < KM; ++k) v[k] = u[0] * eh[k][0] + u[1] * eh[k][1] + u[2] * eh[k][2] + u[3] * eh[k][3];
     v[KM] = u[0] * wgu[0] + u[1] * wgu[1] + u[2] * wgu[2] + u[3] * wgu[3];
-    // 64-lane sums: DPP inside each 16-lane row, then row broadcasts gather
-    // the four row sums into lane 63
+    // 64-lane sums of the KM candidate partials as a reduce-scatter: at each
+    // level a lane keeps one half of its values, adds its partner's copy of
+    // that half and hands the other half over, so the number of values per
+    // lane halves.  The keep rules (bit0^bit2, bit1^bit2, bit2, bit3) make the
+    // half-mirror partner hold the same half as the lane, and the last
+    // levels (rotate by 8 in the row, then swaps across 16 and 32 lanes) pair
+    // lanes with the same index.  Every lane ends with the full sum of
+    // candidate cand_of_lane; the gate partial is summed whole.
+    float w[KM / 2];
 #pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0xB1>(v[k]);
+    for (int m = 0; m < KM / 2; ++m) {
+      const float keep = kc0 ? v[m + KM / 2] : v[m], send = kc0 ? v[m] : v[m + KM / 2];
+      w[m] = keep + dpp_f32<0xB1>(send);  // quad_perm [1,0,3,2]: lane ^ 1
+    }
+    float x[KM / 4];
 #pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x4E>(v[k]);
+    for (int m = 0; m < KM / 4; ++m) {
+      const float keep = kc1 ? w[m + KM / 4] : w[m], send = kc1 ? w[m] : w[m + KM / 4];
+      x[m] = keep + dpp_f32<0x4E>(send);  // quad_perm [2,3,0,1]: lane ^ 2
+    }
+    float y[KM / 8];
 #pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x141>(v[k]);
-#pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += dpp_f32<0x140>(v[k]);
-#pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += dpp_rows<0x142, 0xA>(v[k]);  // row_bcast:15
-#pragma unroll
-    for (int k = 0; k <= KM; ++k) v[k] += dpp_rows<0x143, 0xC>(v[k]);  // row_bcast:31
-    float dk[KM];
-#pragma unroll
-    for (int k = 0; k < KM; ++k) dk[k] = readlane_f32(v[k], 63);
-    float s = readlane_f32(v[KM], 63) + b_g;
+    for (int m = 0; m < KM / 8; ++m) {
+      const float keep = kb2 ? x[m + KM / 8] : x[m], send = kb2 ? x[m] : x[m + KM / 8];
+      y[m] = keep + dpp_f32<0x141>(send);  // row_half_mirror: lane ^ 7 in each 8
+    }
+    float dsum;
+    if constexpr (KM == 16) {
+      const float keep = kb3 ? y[1] : y[0], send = kb3 ? y[0] : y[1];
+      dsum = keep + dpp_f32<0x128>(send);  // row_ror 8: lane ^ 8
+    } else {
+      dsum = y[0] + dpp_f32<0x128>(y[0]);
+    }
+    dsum = swap16_sum(dsum);
+    dsum = swap32_sum(dsum);
+    float gsum = row_sum16(v[KM]);
+    gsum = swap32_sum(swap16_sum(gsum));
+    float s = gsum + b_g;
 #pragma unroll
     for (int f = 0; f < 5; ++f) s += wgphi[f] * phi[f];
     const float g = sig_alpha * sigmoid_rcp(s);
 
-    // refined logits and their argmax (the first maximum: smallest k on ties)
-    float best = __builtin_fmaf(g, dk[0], clu[0]);
-    int kb = 0;
-#pragma unroll
-    for (int k = 1; k < KM; ++k) {
-      const float lt = __builtin_fmaf(g, dk[k], clu[k]);
-      const bool take = k < K && lt > best;
-      best = take ? lt : best;
-      kb = take ? k : kb;
-    }
-    const int kstar = __builtin_amdgcn_readfirstlane(kb);
+    // refined logits and their argmax (the first maximum: smallest k on
+    // ties); every row holds all KM candidates, so row-wide reductions do
+    const float lt = my_cand < K ? __builtin_fmaf(g, dsum, cl_mine) : -INFINITY;
+    const float best = row_max16(lt);
+    int key = my_cand < K && lt == best ? my_cand : KM;
+    key = min(key, dpp_i32<0xB1>(key));
+    key = min(key, dpp_i32<0x4E>(key));
+    key = min(key, dpp_i32<0x141>(key));
+    key = min(key, dpp_i32<0x140>(key));
+    const int kstar = __builtin_amdgcn_readfirstlane(key);
     const int sel = __builtin_amdgcn_readlane(ci_l, kstar);
     prev_x = readlane_f32(xs_l, kstar);
     ptz = sv[64 * (2 + KM + kstar)];
@@ -998,9 +1038,8 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
 
     float ov = g;
     if (want) {
-      float dl = dk[0];
-#pragma unroll
-      for (int k = 1; k < KM; ++k) dl = kd == k ? dk[k] : dl;
+      // candidate kd's sum from a lane that holds it
+      const float dl = __int_as_float(__builtin_amdgcn_ds_bpermute(out_src, __float_as_int(dsum)));
       ov = lane < K ? __builtin_fmaf(g, dl, cl_l) : (lane < 2 * K ? dl : g);
     }
     ov = lane == 63 ? __int_as_float(sel) : ov;
