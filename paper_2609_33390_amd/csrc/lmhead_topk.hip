@@ -587,20 +587,42 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
 // max(a_j, b_{KP-1-j}) is a bitonic sequence holding the KP largest keys of
 // both, and a bitonic half-cleaner network sorts it, so both lanes leave the
 // level with the same merged list.
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int m) {
-  const uint32_t lo = __shfl_xor(static_cast<uint32_t>(v), m, kWave);
-  const uint32_t hi = __shfl_xor(static_cast<uint32_t>(v >> 32), m, kWave);
+// Partner exchange of the butterfly levels, all on the VALU: M = 1, 2 swap
+// lanes inside quads, M = 4 and 8 pair each lane with its mirror in its
+// half-row and row (lane ^ 7, lane ^ 15), and M = 16, 32 use the gfx950
+// lane swaps (lane ^ 16, lane ^ 32).  Applied in the order 1, 2, 4, 8, 16,
+// 32, each level joins disjoint groups of 1, 2, 4, ... lanes, as xor
+// partners would.
+template <int M>
+__device__ __forceinline__ uint32_t lane_xchg(uint32_t v) {
+  if constexpr (M == 1 || M == 2 || M == 4 || M == 8) {
+    constexpr int ctrl = M == 1 ? 0xB1 : M == 2 ? 0x4E : M == 4 ? 0x141 : 0x140;
+    return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), ctrl, 0xF, 0xF, false));
+  } else if constexpr (M == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+    return r[0] == v ? r[1] : r[0];  // one result is the lane's own word
+  } else {
+    static_assert(M == 32, "partner distance");
+    const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+    return r[0] == v ? r[1] : r[0];
+  }
+}
+
+template <int M>
+__device__ __forceinline__ uint64_t lane_xchg_u64(uint64_t v) {
+  const uint32_t lo = lane_xchg<M>(static_cast<uint32_t>(v));
+  const uint32_t hi = lane_xchg<M>(static_cast<uint32_t>(v >> 32));
   return (static_cast<uint64_t>(hi) << 32) | lo;
 }
 
+// Top KP of two descending lists a (in place) and b: c_j = max(a_j,
+// b_{KP-1-j}) is bitonic and holds the KP largest keys of the pair; a bitonic
+// half-cleaner network sorts it.
 template <int KP>
-__device__ __forceinline__ void butterfly_merge(uint64_t (&list)[KP], int m) {
+__device__ __forceinline__ void merge_sorted(uint64_t (&a)[KP], const uint64_t (&b)[KP]) {
   uint64_t c[KP];
 #pragma unroll
-  for (int j = 0; j < KP; ++j) {
-    const uint64_t o = shfl_xor_u64(list[KP - 1 - j], m);
-    c[j] = list[j] > o ? list[j] : o;
-  }
+  for (int j = 0; j < KP; ++j) c[j] = a[j] > b[KP - 1 - j] ? a[j] : b[KP - 1 - j];
 #pragma unroll
   for (int s = KP / 2; s >= 1; s >>= 1) {
 #pragma unroll
@@ -614,7 +636,45 @@ __device__ __forceinline__ void butterfly_merge(uint64_t (&list)[KP], int m) {
     }
   }
 #pragma unroll
-  for (int j = 0; j < KP; ++j) list[j] = c[j];
+  for (int j = 0; j < KP; ++j) a[j] = c[j];
+}
+
+template <int M, int KP>
+__device__ __forceinline__ void butterfly_merge(uint64_t (&list)[KP]) {
+  uint64_t o[KP];
+#pragma unroll
+  for (int j = 0; j < KP; ++j) o[j] = lane_xchg_u64<M>(list[j]);
+  merge_sorted(list, o);
+}
+
+// All 64 lanes end with the wavefront's top KP.
+template <int KP>
+__device__ __forceinline__ void wave_merge(uint64_t (&list)[KP]) {
+  butterfly_merge<1>(list);
+  butterfly_merge<2>(list);
+  butterfly_merge<4>(list);
+  butterfly_merge<8>(list);
+  butterfly_merge<16>(list);
+  butterfly_merge<32>(list);
+}
+
+// Fold parts pt = first, first + step, ... of a row (each a descending list
+// of KP keys, as the LM-head pass writes them) into the thread's list.
+template <int KP>
+__device__ __forceinline__ void fold_parts(uint64_t (&list)[KP], const uint64_t* src, int n_parts, int first,
+                                           int step) {
+  static_assert(KP % 2 == 0, "16-byte loads");
+  for (int pt = first; pt < n_parts; pt += step) {
+    const uint4* p = reinterpret_cast<const uint4*>(src + static_cast<size_t>(pt) * KP);
+    uint64_t kb[KP];
+#pragma unroll
+    for (int q = 0; q < KP / 2; ++q) {
+      const uint4 u = p[q];
+      kb[2 * q] = (static_cast<uint64_t>(u.y) << 32) | u.x;
+      kb[2 * q + 1] = (static_cast<uint64_t>(u.w) << 32) | u.z;
+    }
+    merge_sorted(list, kb);
+  }
 }
 
 // Rows below rows_prop are proposal rows (K candidates out); the rows after
@@ -625,7 +685,8 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
                                                          float* __restrict__ cand_logit,
                                                          int32_t* __restrict__ cand_id,
                                                          int32_t* __restrict__ ver_token) {
-  constexpr int NT = 256, NW = NT / kWave, BATCH = 8;
+  constexpr int NT = 256, NW = NT / kWave;
+  static_assert(NW == 4, "two cross-wave levels");
   __shared__ uint64_t sk[NW][KP];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = blockIdx.x;
@@ -633,19 +694,8 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   uint64_t list[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
-  for (int i0 = tid; i0 < n_keys; i0 += NT * BATCH) {
-    uint64_t kb[BATCH];
-#pragma unroll
-    for (int q = 0; q < BATCH; ++q) {
-      const int i = i0 + q * NT;
-      kb[q] = i < n_keys ? src[i] : 0ull;
-    }
-#pragma unroll
-    for (int q = 0; q < BATCH; ++q)
-      if (kb[q] > list[KP - 1]) list_insert(list, kb[q]);
-  }
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) butterfly_merge(list, m);
+  fold_parts(list, src, n_keys / KP, tid, NT);
+  wave_merge(list);
   if (lane == 0) {
 #pragma unroll
     for (int j = 0; j < KP; ++j) sk[wave][j] = list[j];
@@ -655,8 +705,8 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   // lane l < NW takes wave l's list; two more levels leave the row's list in lane 0
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = lane < NW ? sk[lane][j] : 0ull;
-#pragma unroll
-  for (int m = 1; m < NW; m <<= 1) butterfly_merge(list, m);
+  butterfly_merge<1>(list);
+  butterfly_merge<2>(list);
   if (lane == 0) {
     if (row >= rows_prop) {
       ver_token[row - rows_prop] = key_id(list[0]);
@@ -746,7 +796,8 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
     const int32_t* __restrict__ proposal, const int32_t* __restrict__ cand_id,
     const float* __restrict__ cand_prob, const float* __restrict__ u_accept, float inv_T,
     uint32_t key0, uint32_t key1, int32_t* __restrict__ row_accept, int32_t* __restrict__ row_resample) {
-  constexpr int NT = 256, NW = NT / kWave, BATCH = 8;
+  constexpr int NT = 256, NW = NT / kWave;
+  static_assert(NW == 4, "two cross-wave levels");
   __shared__ uint64_t sk[NW][KP];
   __shared__ float2 s_lse[NT];
   __shared__ float s_logit[kWave + 1];
@@ -759,19 +810,8 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
   uint64_t list[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
-  for (int i0 = tid; i0 < n_keys; i0 += NT * BATCH) {
-    uint64_t kb[BATCH];
-#pragma unroll
-    for (int q = 0; q < BATCH; ++q) {
-      const int i = i0 + q * NT;
-      kb[q] = i < n_keys ? src[i] : 0ull;
-    }
-#pragma unroll
-    for (int q = 0; q < BATCH; ++q)
-      if (kb[q] > list[KP - 1]) list_insert(list, kb[q]);
-  }
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) butterfly_merge(list, m);
+  fold_parts(list, src, n_parts, tid, NT);
+  wave_merge(list);
   if (lane == 0) {
 #pragma unroll
     for (int j = 0; j < KP; ++j) sk[wave][j] = list[j];
@@ -810,8 +850,8 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
   if (wave != 0) return;
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = lane < NW ? sk[lane][j] : 0ull;
-#pragma unroll
-  for (int mm = 1; mm < NW; mm <<= 1) butterfly_merge(list, mm);
+  butterfly_merge<1>(list);
+  butterfly_merge<2>(list);
   if (lane != 0) return;
 
   // (4) decisions, in lane 0, with the accurate exp / log: where p_r and
