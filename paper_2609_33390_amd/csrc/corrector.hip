@@ -854,11 +854,52 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rci, (lds_vptr_t)(st + S::NVEC * 256 + 64), 4, lane * 4, cb, 0, 0);
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rxs, (lds_vptr_t)(st + S::NVEC * 256 + 128), 4, lane * 4, cb, 0, 0);
     };
+    // The gate terms that depend on the row alone (features 0 and 1, and
+    // the candidate-logit half of feature 4) are folded into AZ and AH in
+    // the slot before the recurrence reads it, and the row's part of the
+    // selection gate's pre-activation goes to word 63 of the logit vector
+    // (a lane >= K, which nothing else reads).
+    float cz[4][3], ch[4][3];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const bool ok = 4 * lane + j < ds;
+      const int e = ok ? 4 * lane + j : ds - 1;
+#pragma unroll
+      for (int q = 0; q < 3; ++q) {
+        const int f = q < 2 ? q : 4;
+        const float z = a.FZ[f * ds + e], h = a.FH[f * ds + e];
+        cz[j][q] = ok ? z : 0.f;
+        ch[j][q] = ok ? h : 0.f;
+      }
+    }
+    float wphi[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) wphi[q] = bf16_to_f32(a.w_g[ds + (q < 2 ? q : 4)]);
+    auto prep = [&](int r) {
+      float* st = ring + (r % D) * S::FLOATS;
+      f4_t* sv = reinterpret_cast<f4_t*>(st) + lane;
+      float* sc = st + S::NVEC * 256;
+      const float c0 = sc[0], p0 = c0 - sc[1], p1 = c0 - sc[3];
+      f4_t az = sv[0], ah = sv[64];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        az[j] += cz[j][0] * p0 + cz[j][1] * p1 + cz[j][2] * c0;
+        ah[j] += ch[j][0] * p0 + ch[j][1] * p1 + ch[j][2] * c0;
+      }
+      sv[0] = az;
+      sv[64] = ah;
+      if (lane == 63) sc[63] = a.b_g + wphi[0] * p0 + wphi[1] * p1 + wphi[2] * c0;
+    };
+    // LDS writes complete before the barrier that hands the row over
+    auto handover = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 #pragma unroll
     for (int t = 0; t < D - 1; ++t) issue(t);
+    wait_vm<(D - 2) * S::NDMA>();  // row 0 has landed
+    prep(0);
     for (int i = 0; i < L; ++i) {
-      wait_vm<(D - 2) * S::NDMA>();  // row i has landed
-      wg_barrier();                  // hand slot i over; slot (i-1) % D is free again
+      wait_vm<(D - 3) * S::NDMA>();  // row i + 1 has landed
+      prep(i + 1);
+      handover();                    // hand slot i over; slot (i-1) % D is free again
       issue(i + D - 1);
     }
     wait_vm<0>();  // no copy may land after the workgroup's LDS is released
@@ -948,28 +989,21 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
     for (int k = 0; k < KM; ++k) eh[k] = sv[64 * (2 + k)];
     const float cl_l = sc[lane], xs_l = sc[128 + lane], cl_mine = sc[my_cand];
     const int ci_l = __float_as_int(sc[64 + lane]);
-    float clu[KM];  // every lane reads the same words: the candidate logits as uniform values
-#pragma unroll
-    for (int k = 0; k < KM; ++k) clu[k] = sc[k];
+    const float s_row = sc[63];
     int idu[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) idu[k] = __float_as_int(sc[64 + k]);
 
     float phi[5];
-    phi[0] = clu[0] - clu[1];
-    phi[1] = clu[0] - clu[3];
+    // AZ and AH arrive with the row-only feature terms folded in
     phi[2] = prev_tok == idu[0] ? 1.f : 0.f;
     phi[3] = (prev_tok == idu[0] || prev_tok == idu[1] || prev_tok == idu[2] || prev_tok == idu[3]) ? 1.f : 0.f;
-    phi[4] = clu[0] - prev_x;
 
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       float gz = az[j] + ptz[j], gh = ah[j] + pth[j];
-#pragma unroll
-      for (int f = 0; f < 5; ++f) {
-        gz += fz[j][f] * phi[f];
-        gh += fh[j][f] * phi[f];
-      }
+      gz += fz[j][2] * phi[2] + fz[j][3] * phi[3] - fz[j][4] * prev_x;
+      gh += fh[j][2] * phi[2] + fh[j][3] * phi[3] - fh[j][4] * prev_x;
       const float z = sigmoid_rcp(gz);
       u[j] = (1.f - z) * u[j] + z * gh;
     }
@@ -1015,9 +1049,9 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
     dsum = swap32_sum(dsum);
     float gsum = row_sum16(v[KM]);
     gsum = swap32_sum(swap16_sum(gsum));
-    float s = gsum + b_g;
-#pragma unroll
-    for (int f = 0; f < 5; ++f) s += wgphi[f] * phi[f];
+    // the row's part of the pre-activation (b_g and features 0, 1 and the
+    // logit half of 4) waits in word 63 of the slot's logit vector
+    const float s = gsum + s_row + wgphi[2] * phi[2] + wgphi[3] * phi[3] - wgphi[4] * prev_x;
     const float g = sig_alpha * sigmoid_rcp(s);
 
     // refined logits and their argmax (the first maximum: smallest k on
