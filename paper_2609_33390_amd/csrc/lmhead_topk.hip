@@ -67,7 +67,7 @@ struct TileCfg {
   static_assert(ROWS % (RPI * NW) == 0 && BV % RPI == 0, "DMA instructions must tile the stage");
   static_assert(WV % 16 == 0 && WR % 16 == 0, "wave tile must be a multiple of 16");
   static_assert(NT % BR == 0 && (TPP & (TPP - 1)) == 0, "epilogue thread mapping");
-  static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8), "reduction slice");
+  static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8 || CPR == 16 || CPR == 32), "reduction slice");
   static_assert(EPI_V % (4 * TPP) == 0 && EPI_V >= 32, "epilogue chunking");
   static_assert((STAGES - 2) * NDMA <= 63, "vmcnt range");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
@@ -77,10 +77,12 @@ struct TileCfg {
 // 128-bit LDS read is served 8 lanes at a time; the MFMA operand reads put 8
 // consecutive rows at one chunk in such a group, so the eight rows of every
 // aligned run of 8 must land on eight different 16-byte bank groups (rows are
-// CPR * 16 bytes long, so a bank line of 128 bytes holds 8 / CPR rows).
+// CPR * 16 bytes long: a bank line of 128 bytes holds 8 / CPR rows when CPR
+// < 8, and rows of 8 chunks or more start on the same bank group).
 template <int CPR>
 __device__ __forceinline__ int swz(int r, int c) {
-  return c ^ ((r / (8 / CPR)) & (CPR - 1));
+  if constexpr (CPR >= 8) return c ^ (r & 7);
+  else return c ^ ((r / (8 / CPR)) & (CPR - 1));
 }
 
 // 16-byte slot of chunk c (four logits) in staged logit row p: rows are
@@ -235,10 +237,21 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       const_cast<uint16_t*>(H), static_cast<short>(0), static_cast<int>(static_cast<unsigned>(rows) * d * 2u), 0x00020000);
   const unsigned row_bytes = static_cast<unsigned>(d) * 2u;
   // lane part of a copy's byte offset: row lane / CPR of the instruction's
-  // rows, and the chunk its slot holds (the swizzle repeats every 8 rows, so
-  // it does not depend on the instruction)
+  // rows, and the chunk its slot holds.  The swizzle repeats every 8 rows, so
+  // it does not depend on the instruction when one covers 8 rows or more;
+  // with fewer (slices of 128 bytes per row or more) it depends on the
+  // instruction's first row modulo 8.
   const unsigned lane_voff = static_cast<unsigned>(lane / C::CPR) * row_bytes +
                              static_cast<unsigned>(swz<C::CPR>(lane / C::CPR, lane % C::CPR)) * 16u;
+  auto lane_voff_of = [&](int j) -> unsigned {
+    if constexpr (C::RPI >= 8) {
+      return lane_voff;
+    } else {
+      const int r = j * C::RPI + lane / C::CPR;
+      return static_cast<unsigned>(lane / C::CPR) * row_bytes +
+             static_cast<unsigned>(swz<C::CPR>(r, lane % C::CPR)) * 16u;
+    }
+  };
   auto issue = [&](int g) {
     const int tl = g / nk, kt = g % nk;
     if (tl >= n_tiles) return;
@@ -247,7 +260,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
 #pragma unroll
     for (int i = 0; i < C::NDMA; ++i) {
       const int j = i * C::NW + wave;
-      const unsigned lv = lane_voff;
+      const unsigned lv = lane_voff_of(j);
       if (j * C::RPI < C::BV) {
         const unsigned off = lv + (v0 + static_cast<unsigned>(j * C::RPI)) * row_bytes + k0b;
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rw, (lds_ptr_t)(base + j * 1024), 16, off, 0, 0, 0);
@@ -722,7 +735,11 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   }
 }
 
-using SmallRows = TileCfg<256, 32, 4, 1, 64, 3>;    // <= 32 rows: weight streaming
+// <= 32 rows: weight streaming.  64-row tiles of 256-wide slices read each
+// lm_head row in 512-byte runs, which streams about 3% faster than 256-row
+// tiles of 64-wide slices (128-byte runs) and leaves more tiles for the
+// deferred top-K to hide behind.
+using SmallRows = TileCfg<64, 32, 4, 1, 256, 3>;
 using MidRows = TileCfg<256, 64, 4, 1, 64, 3>;      // <= 64 rows
 using LargeRows = TileCfg<256, 256, 4, 2, 64, 2>;   // many rows: MFMA bound
 
