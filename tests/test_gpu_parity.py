@@ -159,6 +159,9 @@ RAGGED = [
     # vocabularies large enough for one equal share per compute unit (shares
     # of 130-160 rows cut at multiples of 16, partly masked tiles)
     (5, 72, 33333, 7), (50, 136, 40961, 16), (20, 64, 36001, 64),
+    # up to 32 rows the reduction runs in 256-wide slices: several slices
+    # with a tail, exactly one slice, and many slices ending in an 8-wide tail
+    (17, 328, 5000, 8), (32, 584, 70001, 8), (3, 256, 129, 4), (1, 4104, 3001, 8),
 ]
 
 
