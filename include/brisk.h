@@ -11,6 +11,8 @@
  *   brisk_verify_accept  greedy verification: accepted-prefix length and the
  *                        correction token of each block.
  *
+ * brisk_rerank_verify makes the last two in one call.
+ *
  * Conventions shared by every entry point
  *   - Every pointer argument is a DEVICE pointer owned by the caller, except
  *     the brisk_corrector struct itself (host memory, read during the call)
