@@ -251,7 +251,8 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
-              "(the hot path is data parallel: see the sharding notes in DESIGN.md)", file=sys.stderr)
+              "(the hot path is data parallel over sequences: each GPU would run this same step "
+              "on its own share of the batch)", file=sys.stderr)
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
