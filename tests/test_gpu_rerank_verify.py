@@ -39,6 +39,8 @@ CASES = [  # B, L, K, d, V, r (= d_state)
     (2, 130, 16, 64, 800, 256),     # largest single-wavefront shape
     (3, 70, 16, 64, 800, 320),      # d_state > 256: multi-wavefront scan
     (2, 40, 32, 64, 800, 64),       # K > 16: multi-wavefront scan
+    (4, 1, 8, 64, 512, 64),         # one position per block
+    (70, 3, 4, 64, 600, 32),        # many sequences, the smallest K
 ]
 
 
