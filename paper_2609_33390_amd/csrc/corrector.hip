@@ -834,7 +834,7 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
         const_cast<float*>(a.X + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
     // Copies of row i (clamped to the block) into slot i % D.  Candidate slots
     // k >= K repeat candidate K-1, so every row issues exactly NDMA copies and
-    // vmcnt((D-2)*NDMA) always means "every row up to the one D-2 back landed".
+    // vmcnt(n * NDMA) always means "every row but the n last issued landed".
     auto issue = [&](int i) {
       const int ii = i < L ? i : L - 1;
       float* st = ring + (i % D) * S::FLOATS;
@@ -979,6 +979,10 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
   else if (lane == 63) { obase = reinterpret_cast<float*>(a.selected); ostride = 1; }
 
   for (int i = 0; i < L; ++i) {
+    // The copy wave refills the slot of row i - 1 once this barrier passes,
+    // so the reads of that slot (the previous-token vectors, the last ones
+    // of step i - 1) must have returned first.
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
     wg_barrier();  // row i is in slot i % D
     const float* st = ring + (i % D) * S::FLOATS;
     const f4_t* sv = reinterpret_cast<const f4_t*>(st) + lane;  // vector v of the row at sv[64 v]
