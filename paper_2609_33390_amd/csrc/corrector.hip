@@ -931,7 +931,6 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
 #pragma unroll
   for (int f = 0; f < 5; ++f) wgphi[f] = bf16_to_f32(a.w_g[ds + f]);
   const float sig_alpha = sigmoidf_(a.alpha);
-  const float b_g = a.b_g;
   float prev_x = a.X[static_cast<size_t>(a.B) * L * K + b];
   int prev_tok = a.anchor[b];
 
@@ -998,8 +997,10 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
 #pragma unroll
     for (int k = 0; k < 4; ++k) idu[k] = __float_as_int(sc[64 + k]);
 
+    // AZ and AH arrive with the row-only feature terms folded in; features 2
+    // and 3 (the previous token is the top candidate / among the top four)
+    // and the previous cross logit remain
     float phi[5];
-    // AZ and AH arrive with the row-only feature terms folded in
     phi[2] = prev_tok == idu[0] ? 1.f : 0.f;
     phi[3] = (prev_tok == idu[0] || prev_tok == idu[1] || prev_tok == idu[2] || prev_tok == idu[3]) ? 1.f : 0.f;
 
