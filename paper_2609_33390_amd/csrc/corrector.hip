@@ -57,6 +57,9 @@ struct ProjJobs {
 };
 
 constexpr int PJ_BN = 64, PJ_BJ = 64, PJ_BK = 64, PJ_STRIDE = PJ_BK + 8;
+constexpr int PJ_CPR = PJ_BK / 8;        // 16-byte pieces per staged row
+constexpr int PJ_NPC = PJ_BN * PJ_CPR / 256;  // pieces per thread and operand
+static_assert(PJ_BN == PJ_BJ && PJ_NPC >= 1 && PJ_BN * PJ_CPR % 256 == 0, "staging map");
 constexpr int PJ_PF = 2;  // reduction chunks in flight per thread
 
 // One wavefront per cross logit, eight 16-byte loads of each operand in
@@ -136,31 +139,31 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   // past J or n read a valid row whose outputs are never stored, and pieces
   // past d or past the slice (the tail of the last group re-reads the slice's
   // last chunk) are staged as zeros.
-  int arow[2], brow[2], col[2];
+  int arow[PJ_NPC], brow[PJ_NPC], col[PJ_NPC];
 #pragma unroll
-  for (int i = 0; i < 2; ++i) {
+  for (int i = 0; i < PJ_NPC; ++i) {
     const int c = tid + i * 256;
-    const int row = c >> 3;
-    col[i] = (c & 7) * 8;
+    const int row = c / PJ_CPR;
+    col[i] = (c % PJ_CPR) * 8;
     arow[i] = j0 + row < jb.J ? j0 + row : 0;
     const int n = n0 + row;
     brow[i] = n < jb.n ? (jb.idx ? clamp_id(jb.idx[n], jb.n_table) : n) : 0;
   }
-  uint4 ra[PJ_PF][2], rb[PJ_PF][2];
-  auto load = [&](uint4 (&A)[2], uint4 (&Bv)[2], int ch) {
+  uint4 ra[PJ_PF][PJ_NPC], rb[PJ_PF][PJ_NPC];
+  auto load = [&](uint4 (&A)[PJ_NPC], uint4 (&Bv)[PJ_NPC], int ch) {
     const int cc = c_begin + max(min(ch, n_ch - 1), 0);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < PJ_NPC; ++i) {
       const int k = cc * PJ_BK + col[i];
       const int kc = k < d ? k : 0;
       A[i] = *reinterpret_cast<const uint4*>(jb.wt + static_cast<size_t>(arow[i]) * d + kc);
       Bv[i] = *reinterpret_cast<const uint4*>(jb.table + static_cast<size_t>(brow[i]) * d + kc);
     }
   };
-  auto store = [&](const uint4 (&A)[2], const uint4 (&Bv)[2], int ch) {
+  auto store = [&](const uint4 (&A)[PJ_NPC], const uint4 (&Bv)[PJ_NPC], int ch) {
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int row = (tid + i * 256) >> 3;
+    for (int i = 0; i < PJ_NPC; ++i) {
+      const int row = (tid + i * 256) / PJ_CPR;
       const uint32_t m = ch < n_ch && (c_begin + ch) * PJ_BK + col[i] < d ? ~0u : 0u;
       *reinterpret_cast<uint4*>(sA + row * PJ_STRIDE + col[i]) =
           make_uint4(A[i].x & m, A[i].y & m, A[i].z & m, A[i].w & m);
