@@ -692,14 +692,16 @@ __device__ __forceinline__ void fold_parts(uint64_t (&list)[KP], const uint64_t*
 
 // Rows below rows_prop are proposal rows (K candidates out); the rows after
 // them are verifier rows, whose argmax (the top key) goes to ver_token.
-template <int KP>
-__global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restrict__ partial,
-                                                         int rows, int n_keys, int K, int rows_prop,
-                                                         float* __restrict__ cand_logit,
-                                                         int32_t* __restrict__ cand_id,
-                                                         int32_t* __restrict__ ver_token) {
-  constexpr int NT = 256, NW = NT / kWave;
-  static_assert(NW == 4, "two cross-wave levels");
+// NW wavefronts per row: four when there are many parts, one when a row has
+// at most 64 (the batched shapes), which needs no cross-wave stage.
+template <int KP, int NW>
+__global__ __launch_bounds__(64 * NW) void topk_merge_kernel(const uint64_t* __restrict__ partial,
+                                                             int rows, int n_keys, int K, int rows_prop,
+                                                             float* __restrict__ cand_logit,
+                                                             int32_t* __restrict__ cand_id,
+                                                             int32_t* __restrict__ ver_token) {
+  constexpr int NT = NW * kWave;
+  static_assert(NW == 1 || NW == 4, "one wavefront, or two cross-wave levels");
   __shared__ uint64_t sk[NW][KP];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = blockIdx.x;
@@ -709,17 +711,19 @@ __global__ __launch_bounds__(256) void topk_merge_kernel(const uint64_t* __restr
   for (int j = 0; j < KP; ++j) list[j] = 0;
   fold_parts(list, src, n_keys / KP, tid, NT);
   wave_merge(list);
-  if (lane == 0) {
+  if constexpr (NW == 4) {
+    if (lane == 0) {
 #pragma unroll
-    for (int j = 0; j < KP; ++j) sk[wave][j] = list[j];
+      for (int j = 0; j < KP; ++j) sk[wave][j] = list[j];
+    }
+    __syncthreads();
+    if (wave != 0) return;
+    // lane l < NW takes wave l's list; two more levels leave the row's list in lane 0
+#pragma unroll
+    for (int j = 0; j < KP; ++j) list[j] = lane < NW ? sk[lane][j] : 0ull;
+    butterfly_merge<1>(list);
+    butterfly_merge<2>(list);
   }
-  __syncthreads();
-  if (wave != 0) return;
-  // lane l < NW takes wave l's list; two more levels leave the row's list in lane 0
-#pragma unroll
-  for (int j = 0; j < KP; ++j) list[j] = lane < NW ? sk[lane][j] : 0ull;
-  butterfly_merge<1>(list);
-  butterfly_merge<2>(list);
   if (lane == 0) {
     if (row >= rows_prop) {
       ver_token[row - rows_prop] = key_id(list[0]);
@@ -953,8 +957,12 @@ void launch_kp_pass(const Plan& p, const uint16_t* H, const uint16_t* W, int row
 template <int KP>
 void launch_kp_merge(const Plan& p, int rows, int K, int rows_prop, const uint64_t* partial,
                      float* cand_logit, int32_t* cand_id, int32_t* ver_token, hipStream_t s) {
-  hipLaunchKernelGGL((topk_merge_kernel<KP>), dim3(rows), dim3(256), 0, s, partial, rows,
-                     p.n_parts * KP, K, rows_prop, cand_logit, cand_id, ver_token);
+  if (p.n_parts <= kWave)
+    hipLaunchKernelGGL((topk_merge_kernel<KP, 1>), dim3(rows), dim3(kWave), 0, s, partial, rows,
+                       p.n_parts * KP, K, rows_prop, cand_logit, cand_id, ver_token);
+  else
+    hipLaunchKernelGGL((topk_merge_kernel<KP, 4>), dim3(rows), dim3(4 * kWave), 0, s, partial, rows,
+                       p.n_parts * KP, K, rows_prop, cand_logit, cand_id, ver_token);
 }
 
 template <int KP>
