@@ -130,7 +130,7 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wj = wave & 1, wn = wave >> 1;  // 2 x 2 waves, 32 x 32 each
 
-  // Each thread stages two 16-byte pieces of each operand per chunk; its
+  // Each thread stages PJ_NPC 16-byte pieces of each operand per chunk; its
   // rows are fixed, so the gathered table rows are resolved once.  PJ_PF
   // chunks are in flight in registers, so a workgroup with a short slice of
   // the reduction waits about one memory latency, not one per chunk.  Every
@@ -1036,7 +1036,7 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
     // half-mirror partner hold the same half as the lane, and the last
     // levels (rotate by 8 in the row, then swaps across 16 and 32 lanes) pair
     // lanes with the same index.  Every lane ends with the full sum of
-    // candidate cand_of_lane; the gate partial is summed whole.
+    // candidate my_cand; the gate partial is summed whole.
     float w[KM / 2];
 #pragma unroll
     for (int m = 0; m < KM / 2; ++m) {
