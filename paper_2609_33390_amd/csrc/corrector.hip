@@ -56,10 +56,16 @@ struct ProjJobs {
   int d, splits;
 };
 
-constexpr int PJ_BN = 64, PJ_BJ = 64, PJ_BK = 64, PJ_STRIDE = PJ_BK + 8;
+// Tiles are PJ_BN gathered rows x BJ outputs (BJ = 64 or 128, a template
+// argument).  A job with J outputs gathers each of its rows once per output
+// tile, and neighbouring workgroups run on different XCDs, so those re-reads
+// miss in L2: with J = 128, 128-wide tiles halve the gathered traffic, which
+// decides the batched shapes.  Small batches split d instead and keep 64-wide
+// tiles, which give twice as many workgroups.
+constexpr int PJ_BN = 64, PJ_BK = 64, PJ_STRIDE = PJ_BK + 8;
 constexpr int PJ_CPR = PJ_BK / 8;        // 16-byte pieces per staged row
-constexpr int PJ_NPC = PJ_BN * PJ_CPR / 256;  // pieces per thread and operand
-static_assert(PJ_BN == PJ_BJ && PJ_NPC >= 1 && PJ_BN * PJ_CPR % 256 == 0, "staging map");
+constexpr int PJ_NPB = PJ_BN * PJ_CPR / 256;  // gathered-row pieces per thread
+static_assert(PJ_NPB >= 1 && PJ_BN * PJ_CPR % 256 == 0, "staging map");
 constexpr int PJ_PF = 2;  // reduction chunks in flight per thread
 
 // One wavefront per cross logit, eight 16-byte loads of each operand in
@@ -107,30 +113,34 @@ __device__ void cross_dots(const CrossJob& cj, int d) {
   }
 }
 
+template <int BJ>
 __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
+  static_assert(BJ == 64 || BJ == 128, "output tile");
+  constexpr int NPA = BJ * PJ_CPR / 256;  // weight-row pieces per thread
+  constexpr int WJ = BJ / 2, TJ = WJ / 16;  // a wave's outputs and 16-wide fragments
   const int d = jobs.d;
   if (blockIdx.y == kMaxProjJobs) {
     cross_dots(jobs.cross, d);
     return;
   }
   const ProjJob& jb = jobs.job[blockIdx.y];
-  const int n_jt = (jb.J + PJ_BJ - 1) / PJ_BJ;
+  const int n_jt = (jb.J + BJ - 1) / BJ;
   const int n_nt = (jb.n + PJ_BN - 1) / PJ_BN;
   if (static_cast<int>(blockIdx.x) >= n_jt * n_nt) return;
   const int jt = blockIdx.x % n_jt, nt = blockIdx.x / n_jt;
-  const int j0 = jt * PJ_BJ, n0 = nt * PJ_BN;
+  const int j0 = jt * BJ, n0 = nt * PJ_BN;
   const int chunks = (d + PJ_BK - 1) / PJ_BK;
   const int per = (chunks + jobs.splits - 1) / jobs.splits;
   const int c_begin = min(static_cast<int>(blockIdx.z) * per, chunks);
   const int n_ch = min(c_begin + per, chunks) - c_begin;
 
-  __shared__ __align__(16) uint16_t sA[PJ_BJ * PJ_STRIDE];
+  __shared__ __align__(16) uint16_t sA[BJ * PJ_STRIDE];
   __shared__ __align__(16) uint16_t sB[PJ_BN * PJ_STRIDE];
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wj = wave & 1, wn = wave >> 1;  // 2 x 2 waves, 32 x 32 each
+  const int wj = wave & 1, wn = wave >> 1;  // 2 x 2 waves, WJ x 32 each
 
-  // Each thread stages PJ_NPC 16-byte pieces of each operand per chunk; its
+  // Each thread stages NPA + PJ_NPB 16-byte pieces per chunk; its
   // rows are fixed, so the gathered table rows are resolved once.  PJ_PF
   // chunks are in flight in registers, so a workgroup with a short slice of
   // the reduction waits about one memory latency, not one per chunk.  Every
@@ -139,42 +149,51 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   // past J or n read a valid row whose outputs are never stored, and pieces
   // past d or past the slice (the tail of the last group re-reads the slice's
   // last chunk) are staged as zeros.
-  int arow[PJ_NPC], brow[PJ_NPC], col[PJ_NPC];
+  // every piece of a thread has the same column, since 256 is a multiple of
+  // the pieces per row
+  const int col = (tid % PJ_CPR) * 8;
+  int arow[NPA], brow[PJ_NPB];
 #pragma unroll
-  for (int i = 0; i < PJ_NPC; ++i) {
-    const int c = tid + i * 256;
-    const int row = c / PJ_CPR;
-    col[i] = (c % PJ_CPR) * 8;
+  for (int i = 0; i < NPA; ++i) {
+    const int row = (tid + i * 256) / PJ_CPR;
     arow[i] = j0 + row < jb.J ? j0 + row : 0;
-    const int n = n0 + row;
+  }
+#pragma unroll
+  for (int i = 0; i < PJ_NPB; ++i) {
+    const int n = n0 + (tid + i * 256) / PJ_CPR;
     brow[i] = n < jb.n ? (jb.idx ? clamp_id(jb.idx[n], jb.n_table) : n) : 0;
   }
-  uint4 ra[PJ_PF][PJ_NPC], rb[PJ_PF][PJ_NPC];
-  auto load = [&](uint4 (&A)[PJ_NPC], uint4 (&Bv)[PJ_NPC], int ch) {
+  uint4 ra[PJ_PF][NPA], rb[PJ_PF][PJ_NPB];
+  auto load = [&](uint4 (&A)[NPA], uint4 (&Bv)[PJ_NPB], int ch) {
     const int cc = c_begin + max(min(ch, n_ch - 1), 0);
+    const int k = cc * PJ_BK + col;
+    const int kc = k < d ? k : 0;
 #pragma unroll
-    for (int i = 0; i < PJ_NPC; ++i) {
-      const int k = cc * PJ_BK + col[i];
-      const int kc = k < d ? k : 0;
+    for (int i = 0; i < NPA; ++i)
       A[i] = *reinterpret_cast<const uint4*>(jb.wt + static_cast<size_t>(arow[i]) * d + kc);
-      Bv[i] = *reinterpret_cast<const uint4*>(jb.table + static_cast<size_t>(brow[i]) * d + kc);
-    }
-  };
-  auto store = [&](const uint4 (&A)[PJ_NPC], const uint4 (&Bv)[PJ_NPC], int ch) {
 #pragma unroll
-    for (int i = 0; i < PJ_NPC; ++i) {
+    for (int i = 0; i < PJ_NPB; ++i)
+      Bv[i] = *reinterpret_cast<const uint4*>(jb.table + static_cast<size_t>(brow[i]) * d + kc);
+  };
+  auto store = [&](const uint4 (&A)[NPA], const uint4 (&Bv)[PJ_NPB], int ch) {
+    const uint32_t m = ch < n_ch && (c_begin + ch) * PJ_BK + col < d ? ~0u : 0u;
+#pragma unroll
+    for (int i = 0; i < NPA; ++i) {
       const int row = (tid + i * 256) / PJ_CPR;
-      const uint32_t m = ch < n_ch && (c_begin + ch) * PJ_BK + col[i] < d ? ~0u : 0u;
-      *reinterpret_cast<uint4*>(sA + row * PJ_STRIDE + col[i]) =
+      *reinterpret_cast<uint4*>(sA + row * PJ_STRIDE + col) =
           make_uint4(A[i].x & m, A[i].y & m, A[i].z & m, A[i].w & m);
-      *reinterpret_cast<uint4*>(sB + row * PJ_STRIDE + col[i]) =
+    }
+#pragma unroll
+    for (int i = 0; i < PJ_NPB; ++i) {
+      const int row = (tid + i * 256) / PJ_CPR;
+      *reinterpret_cast<uint4*>(sB + row * PJ_STRIDE + col) =
           make_uint4(Bv[i].x & m, Bv[i].y & m, Bv[i].z & m, Bv[i].w & m);
     }
   };
 
-  floatx4 acc[2][2];
+  floatx4 acc[TJ][2];
 #pragma unroll
-  for (int a = 0; a < 2; ++a)
+  for (int a = 0; a < TJ; ++a)
 #pragma unroll
     for (int b = 0; b < 2; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
@@ -197,14 +216,15 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
 #pragma unroll
       for (int kk = 0; kk < PJ_BK; kk += 32) {
         const int koff = kk + (lane >> 4) * 8;
-        bf16x8 a[2], b[2];
+        bf16x8 a[TJ], b[2];
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-          a[t] = *reinterpret_cast<const bf16x8*>(sA + (wj * 32 + t * 16 + (lane & 15)) * PJ_STRIDE + koff);
+        for (int t = 0; t < TJ; ++t)
+          a[t] = *reinterpret_cast<const bf16x8*>(sA + (wj * WJ + t * 16 + (lane & 15)) * PJ_STRIDE + koff);
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
           b[t] = *reinterpret_cast<const bf16x8*>(sB + (wn * 32 + t * 16 + (lane & 15)) * PJ_STRIDE + koff);
-        }
 #pragma unroll
-        for (int x = 0; x < 2; ++x)
+        for (int x = 0; x < TJ; ++x)
 #pragma unroll
           for (int y = 0; y < 2; ++y)
             acc[x][y] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[x], b[y], acc[x][y], 0, 0, 0);
@@ -214,11 +234,11 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   }
   float* out = jb.out + static_cast<size_t>(blockIdx.z) * jb.slice_stride;
 #pragma unroll
-  for (int x = 0; x < 2; ++x)
+  for (int x = 0; x < TJ; ++x)
 #pragma unroll
     for (int y = 0; y < 2; ++y) {
       const int n = n0 + wn * 32 + y * 16 + (lane & 15);
-      const int jb0 = j0 + wj * 32 + x * 16 + (lane >> 4) * 4;
+      const int jb0 = j0 + wj * WJ + x * 16 + (lane >> 4) * 4;
       if (n < jb.n) {
         float* o = out + static_cast<size_t>(n) * jb.J + jb0;
         if (jb0 + 4 <= jb.J && (reinterpret_cast<uintptr_t>(o) & 15u) == 0) {
@@ -1124,7 +1144,7 @@ struct Layout {
   int splits;
 };
 
-int proj_tiles(int n, int J) { return ((J + PJ_BJ - 1) / PJ_BJ) * ((n + PJ_BN - 1) / PJ_BN); }
+int proj_tiles(int n, int J, int bj = 64) { return ((J + bj - 1) / bj) * ((n + PJ_BN - 1) / PJ_BN); }
 
 // Split the gather projections' reduction so that about 1024 workgroups run
 // even when the batch is small; never more than 16 slices.
@@ -1206,9 +1226,11 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   pj.job[3] = ProjJob{hidden, nullptr, rows, c.d_hproj, rows, c.P_h, F(lay.PH), sPH};
   pj.job[4] = ProjJob{ctx_hidden, nullptr, B, ds, B, c.A_h, F(lay.U0), sU0};
   pj.job[5] = ProjJob{tok_embed, anchor_tok, B, ds, V, c.A_e, F(lay.U0) + static_cast<size_t>(B) * ds, sU0};
+  // unsplit (batched) shapes take 128-wide output tiles
+  const int bj = S == 1 ? 128 : 64;
   int max_tiles = 0;
   for (int j = 0; j < kMaxProjJobs; ++j) {
-    const int t = proj_tiles(pj.job[j].n, pj.job[j].J);
+    const int t = proj_tiles(pj.job[j].n, pj.job[j].J, bj);
     max_tiles = t > max_tiles ? t : max_tiles;
   }
   pj.cross = CrossJob{lm_head, hidden, cand_id, anchor_tok, B, L, K, V, F(lay.X)};
@@ -1216,7 +1238,10 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   // (each loops over more when the grid is capped at about 4096 of them)
   const int cross_x = std::min(((NP + 3) / 4 + S - 1) / S, (4096 + S - 1) / S);
   const int gx = std::max(max_tiles, cross_x);
-  hipLaunchKernelGGL(gather_proj_kernel, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
+  if (bj == 128)
+    hipLaunchKernelGGL(gather_proj_kernel<128>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
+  else
+    hipLaunchKernelGGL(gather_proj_kernel<64>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
 
   if (S > 1) {
     SliceArrs sl{};

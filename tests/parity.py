@@ -49,7 +49,8 @@ def check_candidates(cl, ci, ol, tol=SCORE_TOL):
 def check_rerank(gpu, orc, tol=SCORE_TOL):
     """Conditional check: ``orc`` is the oracle run on the GPU's candidates with
     the GPU's selected prefix forced."""
-    assert np.max(np.abs(gpu["refined"] - orc["refined"])) <= tol
+    r_err = np.max(np.abs(gpu["refined"] - orc["refined"]))
+    assert r_err <= tol, (r_err, np.max(np.abs(orc["refined"])))
     g_err = np.abs(gpu["gamma"].astype(np.float64) - orc["gamma"])
     assert np.all(g_err <= 1e-3 * np.abs(orc["gamma"]) + 1e-6), g_err.max()
     dmax = np.max(np.abs(orc["resid"]), axis=1, keepdims=True)

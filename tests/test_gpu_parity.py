@@ -197,11 +197,19 @@ def test_propose_monotone_logits(order):
     check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
 
 
-@pytest.mark.parametrize("B,L,K,d,V,r", [(3, 5, 5, 72, 1000, 32), (2, 9, 4, 136, 600, 96),
-                                          (5, 3, 16, 64, 2000, 320), (70, 2, 8, 64, 512, 256)])
-def test_rerank_ragged(B, L, K, d, V, r):
+@pytest.mark.parametrize("B,L,K,d,V,r,psi", [
+    (3, 5, 5, 72, 1000, 32, 0.3), (2, 9, 4, 136, 600, 96, 0.3), (5, 3, 16, 64, 2000, 320, 0.3),
+    (70, 2, 8, 64, 512, 256, 0.3),
+    # enough candidates that the gathered projections run unsplit, on 128-wide
+    # output tiles: 48 outputs (one partly masked tile), and 160 (a full tile
+    # and a tail) with the multi-wavefront scan.  The second runs 40 positions
+    # at d_state 320, where corrector weights of std 0.3 drive refined scores
+    # to about 4.4e3 and the 1e-2 absolute bound below fp32's reach (a
+    # relative 2e-6); at std 0.1 they stay within about 70.
+    (70, 30, 8, 72, 700, 96, 0.3), (30, 40, 16, 136, 900, 320, 0.1)])
+def test_rerank_ragged(B, L, K, d, V, r, psi):
     wl = synth.Workload("ragged", B=B, L=L, d=d, V=V, K=K, r=r, sigma=0.3, flat_frac=0.5, seed=B + L + K)
-    blk = synth.make_block(wl, "cpu", psi_std=0.3)
+    blk = synth.make_block(wl, "cpu", psi_std=psi)
     io = oracle_inputs(blk)
     g = run_step(_to_dev(blk))
     check_step(blk, g, io)
