@@ -46,6 +46,7 @@ SHAPES = [  # name, B, L, d, V, K
     ("mid", 2, 30, 136, 2049, 8),
     ("large", 5, 60, 64, 3000, 8),     # 300 rows: the large-row tile
     ("k64", 2, 9, 64, 700, 64),
+    ("unsplit", 70, 30, 72, 700, 8),  # 16800 candidates: projections with d unsplit, 128-wide tiles
 ]
 
 
