@@ -192,7 +192,10 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   // (the largest list floor of the position, a lower bound of its KP-th
   // largest key) and queues only the survivors, which the position's list
   // owners then fold.  A tile whose queues overflow takes the full path.
-  constexpr bool kFilt = !SAMPLE && C::BR >= 128 && C::EPI_ALIAS && KP <= 8;  // more keys spill
+  // With 16 keys per list the kernel spills 112 bytes per lane, which costs
+  // far less than the full epilogue on every tile (512 rows x 152064 tokens:
+  // 1026 -> 768 us); longer lists keep the full path.
+  constexpr bool kFilt = !SAMPLE && C::BR >= 128 && C::EPI_ALIAS && KP <= 16;
   float* const s_pthr = reinterpret_cast<float*>(smem + C::POS_OFF);        // [BR]
   int* const s_cnt = reinterpret_cast<int*>(smem + C::POS_OFF + C::BR * 4);  // [BR]
   int* const s_flag = reinterpret_cast<int*>(smem + C::POS_OFF + C::BR * 8);

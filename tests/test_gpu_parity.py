@@ -162,6 +162,8 @@ RAGGED = [
     # up to 32 rows the reduction runs in 256-wide slices: several slices
     # with a tail, exactly one slice, and many slices ending in an 8-wide tail
     (17, 328, 5000, 8), (32, 584, 70001, 8), (3, 256, 129, 4), (1, 4104, 3001, 8),
+    # the large-row tile with 16 keys per list: the filtered epilogue
+    (200, 136, 40000, 16), (513, 72, 9000, 16),
 ]
 
 
@@ -177,13 +179,14 @@ def test_propose_ragged(rows, d, V, K):
     check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
 
 
+@pytest.mark.parametrize("K", [8, 16])
 @pytest.mark.parametrize("order", ["rising", "falling"])
-def test_propose_monotone_logits(order):
+def test_propose_monotone_logits(order, K):
     # 256 rows and V = 2^17 + 37: three vocabulary tiles per workgroup on the
     # large-row tile.  Logits that rise with the token id make every later
     # tile beat the thresholds of the earlier ones (the survivor queues
     # overflow); falling logits leave later tiles with no survivors.
-    rows, d, V, K = 256, 64, (1 << 17) + 37, 8
+    rows, d, V = 256, 64, (1 << 17) + 37
     g = torch.Generator(device="cpu").manual_seed(41)
     u = torch.randn(d, generator=g)
     u = u / u.norm()
