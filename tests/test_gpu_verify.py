@@ -62,9 +62,12 @@ def test_fused_pass_matches_separate_pass_and_oracle(wl_name, sample):
     _say(f"  [{wl_name}] near-tie verifier rows: {near}")
 
 
-@pytest.mark.parametrize("rows_prop,rows_ver", [(0, 40), (40, 0), (1, 1), (100, 300)])
-def test_fused_pass_ragged(rows_prop, rows_ver):
-    wl = synth.Workload("rg", B=1, L=rows_prop + rows_ver, d=136, V=1000, K=5, r=32, sigma=0.3,
+# (100, 300, 16): 400 rows on the large-row tile with 16-key lists, whose
+# epilogue filters survivors
+@pytest.mark.parametrize("rows_prop,rows_ver,K", [(0, 40, 5), (40, 0, 5), (1, 1, 5), (100, 300, 5),
+                                                  (100, 300, 16)])
+def test_fused_pass_ragged(rows_prop, rows_ver, K):
+    wl = synth.Workload("rg", B=1, L=rows_prop + rows_ver, d=136, V=1000, K=K, r=32, sigma=0.3,
                         flat_frac=0.5, seed=rows_prop * 7 + rows_ver)
     blk = synth.make_block(wl, "cuda")
     cl, ci, vt = brisk.propose_verify(blk.H, blk.W, rows_prop, wl.K)
