@@ -306,6 +306,85 @@ def test_feature5_uses_full_vocab_logit_and_gate_uses_raw_features():
     assert np.isclose(out["gamma"][0], 1 / (1 + np.exp(-0.125)), atol=1e-7)
 
 
+def test_init_reads_anchor_embedding_through_A_e():
+    """u_0 = tanh(A_h h_c + A_e E(x_0)) (Init, reading R3) with h_c = 0 and only
+    A_e[1, 1] = 1 gives u_0 = (0, tanh E[x_0, 1]) = (0, tanh 1.5).  z = 0 keeps
+    u_i = u_0 at both steps; W_s = I and W_c reading the first two coordinates
+    give d_k = tanh(1.5) * W[v_k, 1], so candidate 2 (W[2, 1] = 1) wins.
+
+    Mutations this fails under: dropping the A_e term (u_0 = 0, residual 0);
+    applying A_e to the LM-head row W[x_0] instead of the input embedding
+    E[x_0] (W[x_0, 1] = -2, so the residual flips sign and top-1 stays)."""
+    t = Tiny()
+    t.psi["A_e"][1, 1] = 1.0
+    t.Ef[5, 1] = 1.5                                 # x_0 = 5
+    t.Wf[5, 1] = -2.0                                # a different value in E_out's row of x_0
+    t.psi["pos_emb"][:, 0] = 1.0
+    t.psi["W_z"][:, 2] = -80.0                       # z -> 0: u_i = u_0
+    t.b_g = 60.0                                     # gamma = sigmoid(0) * 1 = 1/2
+    t.Wf[2, 1] = 1.0
+    out = t.run()
+    u0 = np.tanh(1.5)
+    for i in range(2):
+        assert np.allclose(out["resid"][i], [0.0, 0.0, u0, 0.0], atol=1e-12)
+    assert np.allclose(out["refined"][0], [3.0, 2.875, 2.75 + 0.5 * u0, 2.5], atol=1e-6)
+    assert out["selected"].tolist() == [[2, 2]]
+
+
+def test_hidden_projection_reads_the_current_row():
+    """Slot 0 of x_hat is P_h m_i (reading R5).  With P_h reading coordinate 0,
+    z = 1 and W_h copying slot 0 into the first state element, u_i = (m_i[0], 0)
+    and d_k = m_i[0] * W[v_k, 0].  The two rows differ (m_1[0] = 1,
+    m_2[0] = -2): residuals (0, 0.5, -0.5, 0) then (0, -1, 1, 0), selections 1
+    then 2.
+
+    Mutations this fails under: feeding m_{i-1} or m_{i+1} instead of m_i
+    (the rows swap, at step 1 through numpy's wrap-around), or leaving the
+    slot out (residual 0, top-1 at both steps)."""
+    t = Tiny()
+    t.H[0, 0], t.H[1, 0] = 1.0, -2.0
+    t.psi["P_h"][0, 0] = 1.0
+    t.psi["pos_emb"][:, 0] = 1.0
+    t.psi["W_z"][:, 2] = 80.0                        # z -> 1
+    t.psi["W_h"][:, 0] = [1.0, 0.0]                  # u_i = (x_hat_0, 0)
+    t.Wf[1, 0], t.Wf[2, 0] = 0.5, -0.5
+    t.b_g = 60.0                                     # gamma = 1/2
+    out = t.run()
+    assert np.allclose(out["resid"][0], [0.0, 0.5, -0.5, 0.0], atol=1e-12)
+    assert np.allclose(out["resid"][1], [0.0, -1.0, 1.0, 0.0], atol=1e-12)
+    assert np.allclose(out["refined"][1], [3.0, 2.375, 3.25, 2.5], atol=1e-6)
+    assert out["selected"].tolist() == [[1, 2]]
+
+
+def test_feature_projection_slot():
+    """Slot 4 of x_hat is P_phi phi_i (readings R5, R6).  P_phi = [1, -1, 1/2,
+    1/4, 1/4] and W_h copying slot 4 into the first state element give
+    u_i = (P_phi phi_i, 0) at z = 1, and d_k = u_i[0] * W[v_k, 0] with only
+    W[1, 0] = 1.  Step 1: phi = (1/8, 1/2, 0, 0, 3) (x_0 = 5 is no candidate,
+    its logit is 0), P_phi phi = 3/8.  Step 2: x_1 = 1 is in the top 4 but not
+    top 1, phi = (1/8, 1/2, 0, 1, 3), P_phi phi = 5/8.
+
+    Mutations this fails under: leaving the slot out (residual 0, top-1
+    selected), any reordering of the five features before P_phi (for example
+    swapping the two indicator features gives 7/8 at step 2, reversing them
+    gives other values at both steps), or gating the projection instead of the
+    raw features."""
+    t = Tiny()
+    t.psi["P_phi"][0] = [1.0, -1.0, 0.5, 0.25, 0.25]
+    t.psi["pos_emb"][:, 0] = 1.0
+    t.psi["W_z"][:, 2] = 80.0                        # z -> 1
+    t.psi["W_h"][:, 4] = [1.0, 0.0]                  # u_i = (P_phi phi_i, 0)
+    t.Wf[1, 0] = 1.0
+    t.b_g = 60.0                                     # gamma = 1/2
+    out = t.run()
+    assert np.allclose(out["phi"][0], [0.125, 0.5, 0.0, 0.0, 3.0], atol=1e-7)
+    assert np.allclose(out["phi"][1], [0.125, 0.5, 0.0, 1.0, 3.0], atol=1e-7)
+    assert np.allclose(out["resid"][0], [0.0, 0.375, 0.0, 0.0], atol=1e-12)
+    assert np.allclose(out["resid"][1], [0.0, 0.625, 0.0, 0.0], atol=1e-12)
+    assert np.allclose(out["gamma"], 0.5, atol=1e-12)
+    assert out["selected"].tolist() == [[1, 1]]
+
+
 def test_unique_self_consistent_path_is_the_greedy_one():
     """Brute force over all K^L candidate paths of a small block: run the
     corrector teacher-forced on each path; exactly one path chooses itself at
