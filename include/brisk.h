@@ -161,7 +161,9 @@ int brisk_rerank_workspace_size(const brisk_corrector* c, int32_t B, int32_t L, 
  *   resid       [B*L, K] fp32   out, nullable: residual <W_s u_i, W_c E_out(v)>
  *
  * Limits: 4 <= K <= 64 (the features read the top-4), 1 <= L <= max_L,
- * B*L <= 2^20, L*(2+3K)*d_state*4 below 2^31 bytes.
+ * B*L <= 2^20, and one sequence's step blocks L*(2+3K)*max(256, d_state)*4
+ * below 2^31 bytes (each step vector is padded to at least 256 floats);
+ * beyond that the call returns BRISK_ERR_UNSUPPORTED.
  */
 int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
                  const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,

@@ -136,17 +136,44 @@ def _check(status: int, where: str) -> None:
         raise BriskError(status, where)
 
 
-def _dev_tensor(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: int) -> None:
+def _dev_tensor(t: torch.Tensor, name: str, dtype: torch.dtype, ndim: Optional[int] = None, *,
+                shape: Optional[Tuple[int, ...]] = None, device: Optional[torch.device] = None) -> None:
+    """Checks a tensor before its pointer goes to the library: type, dtype,
+    dimension count or exact shape, contiguity, a HIP device, and (when
+    ``device`` is given) the same device as the call's other tensors.  A
+    wrong shape would otherwise let a kernel read or write past the buffer."""
     if not isinstance(t, torch.Tensor):
         raise TypeError(f"{name} must be a torch.Tensor")
-    if t.device.type != "cuda":
-        raise ValueError(f"{name} must live on a HIP device, got {t.device}")
     if t.dtype != dtype:
         raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
-    if t.dim() != ndim:
+    if shape is not None:
+        if tuple(t.shape) != tuple(shape):
+            raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    elif ndim is not None and t.dim() != ndim:
         raise ValueError(f"{name} must have {ndim} dims, got shape {tuple(t.shape)}")
     if not t.is_contiguous():
         raise ValueError(f"{name} must be contiguous")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must live on a HIP device, got {t.device}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the call's other tensors on {device}")
+
+
+def _ws_bytes(ws: torch.Tensor, device: torch.device, need: int, name: str = "workspace") -> int:
+    """Size in bytes of a caller's workspace, after checking that it is a
+    contiguous tensor on the call's device and holds at least ``need`` bytes."""
+    if not isinstance(ws, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not ws.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if ws.device.type != "cuda":
+        raise ValueError(f"{name} must live on a HIP device, got {ws.device}")
+    if ws.device != device:
+        raise ValueError(f"{name} is on {ws.device}, the call's other tensors on {device}")
+    nbytes = ws.numel() * ws.element_size()
+    if nbytes < need:
+        raise ValueError(f"{name} holds {nbytes} bytes, the call needs {need}")
+    return nbytes
 
 
 def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
@@ -174,6 +201,17 @@ def _workspace(device: torch.device, nbytes: int, tag: str) -> torch.Tensor:
 
 
 # ----------------------------------------------------------------- propose
+def _lmhead_operands(hidden: torch.Tensor, lm_head: torch.Tensor):
+    """(rows, d, V, device) of a hidden-state block and an LM head, checked."""
+    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
+    dev = hidden.device
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2, device=dev)
+    rows, d = hidden.shape
+    if lm_head.shape[1] != d:
+        raise ValueError("hidden and lm_head disagree on d")
+    return rows, d, lm_head.shape[0], dev
+
+
 def propose_workspace_size(rows: int, d: int, V: int, K: int) -> int:
     out = _sz()
     _check(lib().brisk_propose_workspace_size(rows, d, V, K, ctypes.byref(out)),
@@ -186,23 +224,17 @@ def propose_block(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, *,
                   workspace: Optional[torch.Tensor] = None, stream=None
                   ) -> Tuple[torch.Tensor, torch.Tensor]:
     """Ordered top-K candidates of every row: (cand_logit [rows,K] fp32, cand_id [rows,K] int32)."""
-    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
-    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
-    rows, d = hidden.shape
-    V = lm_head.shape[0]
-    if lm_head.shape[1] != d:
-        raise ValueError("hidden and lm_head disagree on d")
-    dev = hidden.device
+    rows, d, V, dev = _lmhead_operands(hidden, lm_head)
     if cand_logit is None:
         cand_logit = torch.empty(rows, K, dtype=torch.float32, device=dev)
     if cand_id is None:
         cand_id = torch.empty(rows, K, dtype=torch.int32, device=dev)
-    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
-    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, shape=(rows, K), device=dev)
+    _dev_tensor(cand_id, "cand_id", torch.int32, shape=(rows, K), device=dev)
     need = propose_workspace_size(rows, d, V, K)
     ws = workspace if workspace is not None else _workspace(dev, need, "propose")
     st = lib().brisk_propose_block(_ptr(hidden), _ptr(lm_head), rows, d, V, K, _ptr(cand_logit),
-                                   _ptr(cand_id), _ptr(ws), ws.numel() * ws.element_size(),
+                                   _ptr(cand_id), _ptr(ws), _ws_bytes(ws, dev, need),
                                    _stream_ptr(dev, stream))
     _check(st, "brisk_propose_block")
     return cand_logit, cand_id
@@ -211,26 +243,22 @@ def propose_block(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, *,
 def propose_lmhead(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, workspace: torch.Tensor, *,
                    stream=None) -> None:
     """The LM-head pass of propose_block alone: per-share ordered keys into ``workspace``."""
-    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
-    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
-    rows, d = hidden.shape
-    V = lm_head.shape[0]
-    if lm_head.shape[1] != d:
-        raise ValueError("hidden and lm_head disagree on d")
+    rows, d, V, dev = _lmhead_operands(hidden, lm_head)
+    need = propose_workspace_size(rows, d, V, K)
     st = lib().brisk_propose_lmhead(_ptr(hidden), _ptr(lm_head), rows, d, V, K, _ptr(workspace),
-                                    workspace.numel() * workspace.element_size(),
-                                    _stream_ptr(hidden.device, stream))
+                                    _ws_bytes(workspace, dev, need), _stream_ptr(dev, stream))
     _check(st, "brisk_propose_lmhead")
 
 
 def propose_merge(rows: int, V: int, K: int, workspace: torch.Tensor, cand_logit: torch.Tensor,
                   cand_id: torch.Tensor, *, stream=None) -> None:
     """The merge of propose_block alone: candidates from the keys a propose_lmhead left."""
-    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
-    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, shape=(rows, K))
+    dev = cand_logit.device
+    _dev_tensor(cand_id, "cand_id", torch.int32, shape=(rows, K), device=dev)
+    need = propose_workspace_size(rows, 8, V, K)   # the key layout does not depend on d
     st = lib().brisk_propose_merge(rows, V, K, _ptr(cand_logit), _ptr(cand_id), _ptr(workspace),
-                                   workspace.numel() * workspace.element_size(),
-                                   _stream_ptr(cand_logit.device, stream))
+                                   _ws_bytes(workspace, dev, need), _stream_ptr(dev, stream))
     _check(st, "brisk_propose_merge")
 
 
@@ -242,14 +270,29 @@ class Corrector:
         missing = [n for n in PSI_FIELDS if n not in tensors]
         if missing:
             raise ValueError(f"missing corrector tensors: {missing}")
+        for n in PSI_FIELDS:
+            v = tensors[n]
+            if not isinstance(v, torch.Tensor) or v.dim() != (1 if n == "w_g" else 2):
+                raise ValueError(f"{n} must be a {1 if n == 'w_g' else 2}-d tensor")
         self.t = {n: tensors[n].contiguous() for n in PSI_FIELDS}
-        for n, v in self.t.items():
-            _dev_tensor(v, n, torch.bfloat16, 1 if n == "w_g" else 2)
         self.alpha, self.b_g = float(alpha), float(b_g)
-        ds = self.t["A_h"].shape[0]
-        self.dims = dict(d_state=ds, d_hproj=self.t["P_h"].shape[0], d_tproj=self.t["P_e"].shape[0],
-                         d_pos=self.t["pos_emb"].shape[1], d_feat=self.t["P_phi"].shape[0],
-                         rank=self.t["W_s"].shape[0], max_L=self.t["pos_emb"].shape[0])
+        t = self.t
+        ds, self.d = t["A_h"].shape
+        self.device = t["A_h"].device
+        self.dims = dict(d_state=ds, d_hproj=t["P_h"].shape[0], d_tproj=t["P_e"].shape[0],
+                         d_pos=t["pos_emb"].shape[1], d_feat=t["P_phi"].shape[0],
+                         rank=t["W_s"].shape[0], max_L=t["pos_emb"].shape[0])
+        dm = self.dims
+        d_in = dm["d_hproj"] + dm["d_tproj"] + dm["d_pos"] + dm["d_feat"]
+        want = {"A_h": (ds, self.d), "A_e": (ds, self.d), "P_h": (dm["d_hproj"], self.d),
+                "P_e": (dm["d_tproj"], self.d), "pos_emb": (dm["max_L"], dm["d_pos"]),
+                "P_phi": (dm["d_feat"], 5), "W_z": (ds, d_in), "W_h": (ds, d_in),
+                "W_s": (dm["rank"], ds), "W_c": (dm["rank"], self.d), "w_g": (ds + 5,)}
+        for n in PSI_FIELDS:        # every shape first, then dtypes and devices
+            if tuple(t[n].shape) != want[n]:
+                raise ValueError(f"{n} must have shape {want[n]}, got {tuple(t[n].shape)}")
+        for n in PSI_FIELDS:
+            _dev_tensor(t[n], n, torch.bfloat16, shape=want[n], device=self.device)
         self._c = _CorrectorC(**self.dims, **{n: _ptr(self.t[n]) for n in PSI_FIELDS},
                               alpha=self.alpha, b_g=self.b_g)
 
@@ -267,20 +310,26 @@ def rerank_workspace_size(corr: Corrector, B: int, L: int, K: int) -> int:
 
 def _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id, B, L,
                  want_scores, selected, refined, gamma, resid, workspace):
+    rows = B * L
     _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
-    _dev_tensor(ctx_hidden, "ctx_hidden", torch.bfloat16, 2)
-    _dev_tensor(anchor_tok, "anchor_tok", torch.int32, 1)
-    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
-    _dev_tensor(tok_embed, "tok_embed", torch.bfloat16, 2)
-    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
-    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
-    rows, d = hidden.shape
-    V, K = lm_head.shape[0], cand_id.shape[1]
-    if rows != B * L or cand_id.shape[0] != rows or tuple(cand_logit.shape) != (rows, K):
-        raise ValueError("row counts disagree with B*L")
-    if ctx_hidden.shape != (B, d) or anchor_tok.shape[0] != B or tok_embed.shape != lm_head.shape:
-        raise ValueError("context / anchor / embedding shapes disagree")
     dev = hidden.device
+    if hidden.shape[0] != rows:
+        raise ValueError(f"hidden has {hidden.shape[0]} rows, B*L = {rows}")
+    d = hidden.shape[1]
+    if d != corr.d or corr.device != dev:
+        raise ValueError(f"the corrector was built for d = {corr.d} on {corr.device}, "
+                         f"the hidden states have d = {d} on {dev}")
+    _dev_tensor(ctx_hidden, "ctx_hidden", torch.bfloat16, shape=(B, d), device=dev)
+    _dev_tensor(anchor_tok, "anchor_tok", torch.int32, shape=(B,), device=dev)
+    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2, device=dev)
+    V = lm_head.shape[0]
+    if lm_head.shape[1] != d:
+        raise ValueError("hidden and lm_head disagree on d")
+    _dev_tensor(tok_embed, "tok_embed", torch.bfloat16, shape=(V, d), device=dev)
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2, device=dev)
+    K = cand_id.shape[1]
+    _dev_tensor(cand_id, "cand_id", torch.int32, shape=(rows, K), device=dev)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, shape=(rows, K), device=dev)
     if selected is None:
         selected = torch.empty(B, L, dtype=torch.int32, device=dev)
     if want_scores:
@@ -290,13 +339,18 @@ def _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_
             gamma = torch.empty(rows, dtype=torch.float32, device=dev)
         if resid is None:
             resid = torch.empty(rows, K, dtype=torch.float32, device=dev)
+    _dev_tensor(selected, "selected", torch.int32, shape=(B, L), device=dev)
+    for name, t, shp in (("refined", refined, (rows, K)), ("gamma", gamma, (rows,)), ("resid", resid, (rows, K))):
+        if t is not None:
+            _dev_tensor(t, name, torch.float32, shape=shp, device=dev)
     need = rerank_workspace_size(corr, B, L, K)
     ws = workspace if workspace is not None else _workspace(dev, need, "rerank")
+    ws_n = _ws_bytes(ws, dev, need)
     out = {"selected": selected}
     for k, v in (("refined", refined), ("gamma", gamma), ("resid", resid)):
         if v is not None:
             out[k] = v
-    return K, d, V, dev, ws, out
+    return K, d, V, dev, ws, ws_n, out
 
 
 def rerank(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anchor_tok: torch.Tensor,
@@ -307,14 +361,14 @@ def rerank(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anch
            workspace: Optional[torch.Tensor] = None, stream=None) -> Dict[str, torch.Tensor]:
     """Run the corrector; returns {"selected": [B,L] int32} plus "refined", "gamma",
     "resid" when ``want_scores`` (or when the caller passes those buffers)."""
-    K, d, V, dev, ws, out = _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
-                                         cand_logit, cand_id, B, L, want_scores, selected, refined,
-                                         gamma, resid, workspace)
+    K, d, V, dev, ws, ws_n, out = _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                                               cand_logit, cand_id, B, L, want_scores, selected, refined,
+                                               gamma, resid, workspace)
     st = lib().brisk_rerank(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
                             _ptr(anchor_tok), _ptr(lm_head), _ptr(tok_embed), _ptr(cand_logit),
                             _ptr(cand_id), B, L, K, d, V, _ptr(out["selected"]), _ptr(out.get("refined")),
-                            _ptr(out.get("gamma")), _ptr(out.get("resid")), _ptr(ws),
-                            ws.numel() * ws.element_size(), _stream_ptr(dev, stream))
+                            _ptr(out.get("gamma")), _ptr(out.get("resid")), _ptr(ws), ws_n,
+                            _stream_ptr(dev, stream))
     _check(st, "brisk_rerank")
     return out
 
@@ -329,22 +383,22 @@ def rerank_verify(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tenso
                   stream=None) -> Dict[str, torch.Tensor]:
     """:func:`rerank` then :func:`verify_accept` on its selections, in one call.
     Returns the rerank outputs plus "accept_len" and "correction" [B] int32."""
-    _dev_tensor(verifier, "verifier", torch.int32, 2)
-    if tuple(verifier.shape) != (B, L):
-        raise ValueError("verifier must be [B, L]")
-    K, d, V, dev, ws, out = _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
-                                         cand_logit, cand_id, B, L, want_scores, selected, refined,
-                                         gamma, resid, workspace)
+    K, d, V, dev, ws, ws_n, out = _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                                               cand_logit, cand_id, B, L, want_scores, selected, refined,
+                                               gamma, resid, workspace)
+    _dev_tensor(verifier, "verifier", torch.int32, shape=(B, L), device=dev)
     if accept_len is None:
         accept_len = torch.empty(B, dtype=torch.int32, device=dev)
     if correction is None:
         correction = torch.empty(B, dtype=torch.int32, device=dev)
+    _dev_tensor(accept_len, "accept_len", torch.int32, shape=(B,), device=dev)
+    _dev_tensor(correction, "correction", torch.int32, shape=(B,), device=dev)
     st = lib().brisk_rerank_verify(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
                                    _ptr(anchor_tok), _ptr(lm_head), _ptr(tok_embed), _ptr(cand_logit),
                                    _ptr(cand_id), _ptr(verifier), B, L, K, d, V, _ptr(out["selected"]),
                                    _ptr(out.get("refined")), _ptr(out.get("gamma")), _ptr(out.get("resid")),
-                                   _ptr(accept_len), _ptr(correction), _ptr(ws),
-                                   ws.numel() * ws.element_size(), _stream_ptr(dev, stream))
+                                   _ptr(accept_len), _ptr(correction), _ptr(ws), ws_n,
+                                   _stream_ptr(dev, stream))
     _check(st, "brisk_rerank_verify")
     out["accept_len"] = accept_len
     out["correction"] = correction
@@ -357,15 +411,15 @@ def verify_accept(proposal: torch.Tensor, verifier: torch.Tensor, *,
                   stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """(accept_len [B] int32, correction [B] int32; -1 where the block is fully accepted)."""
     _dev_tensor(proposal, "proposal", torch.int32, 2)
-    _dev_tensor(verifier, "verifier", torch.int32, 2)
-    if proposal.shape != verifier.shape:
-        raise ValueError("proposal and verifier shapes differ")
     B, L = proposal.shape
     dev = proposal.device
+    _dev_tensor(verifier, "verifier", torch.int32, shape=(B, L), device=dev)
     if accept_len is None:
         accept_len = torch.empty(B, dtype=torch.int32, device=dev)
     if correction is None:
         correction = torch.empty(B, dtype=torch.int32, device=dev)
+    _dev_tensor(accept_len, "accept_len", torch.int32, shape=(B,), device=dev)
+    _dev_tensor(correction, "correction", torch.int32, shape=(B,), device=dev)
     st = lib().brisk_verify_accept(_ptr(proposal), _ptr(verifier), B, L, _ptr(accept_len),
                                    _ptr(correction), _stream_ptr(dev, stream))
     _check(st, "brisk_verify_accept")
@@ -384,11 +438,12 @@ def accept_profile(accept_len: torch.Tensor, M: int, *, eps: float = 0.0,
            "brisk_accept_profile_workspace_size")
     if workspace is None:
         workspace = _workspace(dev, nbytes.value, "profile")
+    ws_n = _ws_bytes(workspace, dev, nbytes.value)
     out = {k: torch.empty(M, dtype=torch.float64, device=dev) for k in ("a", "w_raw", "w")}
     out["tpf_fpt"] = torch.empty(2, dtype=torch.float64, device=dev)
     st = lib().brisk_accept_profile(_ptr(accept_len) if n > 0 else None, n, M, float(eps),
                                     _ptr(out["a"]), _ptr(out["w_raw"]), _ptr(out["w"]),
-                                    _ptr(out["tpf_fpt"]), _ptr(workspace), workspace.numel(),
+                                    _ptr(out["tpf_fpt"]), _ptr(workspace), ws_n,
                                     _stream_ptr(dev, stream))
     _check(st, "brisk_accept_profile")
     return out
@@ -401,20 +456,19 @@ def propose_verify(hidden: torch.Tensor, lm_head: torch.Tensor, rows_prop: int, 
     """One LM-head pass: the first ``rows_prop`` rows of ``hidden`` get ordered
     top-K candidates, the remaining rows their argmax token.
     Returns (cand_logit [rows_prop, K], cand_id [rows_prop, K], ver_token [rows_ver])."""
-    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
-    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
-    rows, d = hidden.shape
-    V = lm_head.shape[0]
+    rows, d, V, dev = _lmhead_operands(hidden, lm_head)
     rows_ver = rows - rows_prop
     if rows_prop < 0 or rows_ver < 0:
         raise ValueError("rows_prop must lie in [0, hidden rows]")
-    dev = hidden.device
     if cand_logit is None:
         cand_logit = torch.empty(rows_prop, K, dtype=torch.float32, device=dev)
     if cand_id is None:
         cand_id = torch.empty(rows_prop, K, dtype=torch.int32, device=dev)
     if ver_token is None:
         ver_token = torch.empty(rows_ver, dtype=torch.int32, device=dev)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, shape=(rows_prop, K), device=dev)
+    _dev_tensor(cand_id, "cand_id", torch.int32, shape=(rows_prop, K), device=dev)
+    _dev_tensor(ver_token, "ver_token", torch.int32, shape=(rows_ver,), device=dev)
     nbytes = _sz(0)
     _check(lib().brisk_propose_verify_workspace_size(rows_prop, rows_ver, d, V, K, ctypes.byref(nbytes)),
            "brisk_propose_verify_workspace_size")
@@ -422,8 +476,8 @@ def propose_verify(hidden: torch.Tensor, lm_head: torch.Tensor, rows_prop: int, 
     st = lib().brisk_propose_verify(_ptr(hidden), _ptr(lm_head), rows_prop, rows_ver, d, V, K,
                                     _ptr(cand_logit) if rows_prop else None,
                                     _ptr(cand_id) if rows_prop else None,
-                                    _ptr(ver_token) if rows_ver else None, _ptr(ws), ws.numel(),
-                                    _stream_ptr(dev, stream))
+                                    _ptr(ver_token) if rows_ver else None, _ptr(ws),
+                                    _ws_bytes(ws, dev, nbytes.value), _stream_ptr(dev, stream))
     _check(st, "brisk_propose_verify")
     return cand_logit, cand_id, ver_token
 
@@ -432,11 +486,9 @@ def verify_commit(proposal: torch.Tensor, verifier: torch.Tensor, *, stream=None
                   ) -> Tuple[torch.Tensor, torch.Tensor, torch.Tensor]:
     """(accept_len [B], committed [B, L + 1] padded with -1, n_committed [B])."""
     _dev_tensor(proposal, "proposal", torch.int32, 2)
-    _dev_tensor(verifier, "verifier", torch.int32, 2)
-    if proposal.shape != verifier.shape:
-        raise ValueError("proposal and verifier shapes differ")
     B, L = proposal.shape
     dev = proposal.device
+    _dev_tensor(verifier, "verifier", torch.int32, shape=(B, L), device=dev)
     acc = torch.empty(B, dtype=torch.int32, device=dev)
     committed = torch.empty(B, L + 1, dtype=torch.int32, device=dev)
     n = torch.empty(B, dtype=torch.int32, device=dev)
@@ -451,15 +503,16 @@ def corrector_loss(ver_hidden: torch.Tensor, lm_head: torch.Tensor, cand_id: tor
                    B: int, L: int, *, beta: float = 0.01, stream=None) -> Dict[str, torch.Tensor]:
     """Per-position losses ``loss_pos``, ``ce``, ``kl`` [B*L] and ``loss_mean``
     [2] = (mean over reached positions, their count)."""
-    _dev_tensor(ver_hidden, "ver_hidden", torch.bfloat16, 2)
-    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
-    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
-    _dev_tensor(cand_logit, "cand_logit", torch.float32, 2)
-    _dev_tensor(refined, "refined", torch.float32, 2)
-    _dev_tensor(accept_len, "accept_len", torch.int32, 1)
-    rows, K = cand_id.shape
-    d, V = ver_hidden.shape[1], lm_head.shape[0]
-    dev = ver_hidden.device
+    rows = B * L
+    nrows, d, V, dev = _lmhead_operands(ver_hidden, lm_head)
+    if nrows != rows:
+        raise ValueError(f"ver_hidden has {nrows} rows, B*L = {rows}")
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2, device=dev)
+    K = cand_id.shape[1]
+    _dev_tensor(cand_id, "cand_id", torch.int32, shape=(rows, K), device=dev)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, shape=(rows, K), device=dev)
+    _dev_tensor(refined, "refined", torch.float32, shape=(rows, K), device=dev)
+    _dev_tensor(accept_len, "accept_len", torch.int32, shape=(B,), device=dev)
     out = {k: torch.empty(rows, dtype=torch.float32, device=dev) for k in ("loss_pos", "ce", "kl")}
     out["loss_mean"] = torch.empty(2, dtype=torch.float32, device=dev)
     st = lib().brisk_corrector_loss(_ptr(ver_hidden), _ptr(lm_head), _ptr(cand_id), _ptr(cand_logit),
@@ -477,21 +530,22 @@ def spec_verify(ver_hidden: torch.Tensor, lm_head: torch.Tensor, proposal: torch
     """Stochastic verification: ``accept_len``, ``correction`` [B] and the
     per-position ``row_accept``, ``row_resample`` [B*L].  ``cand_prob=None``
     is the greedy proposer (pi = point mass at the proposal)."""
-    _dev_tensor(ver_hidden, "ver_hidden", torch.bfloat16, 2)
-    _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2)
-    _dev_tensor(proposal, "proposal", torch.int32, 2)
-    _dev_tensor(cand_id, "cand_id", torch.int32, 2)
-    if cand_prob is not None:
-        _dev_tensor(cand_prob, "cand_prob", torch.float32, 2)
-    _dev_tensor(u_accept, "u_accept", torch.float32, 1)
+    rows, d, V, dev = _lmhead_operands(ver_hidden, lm_head)
+    _dev_tensor(proposal, "proposal", torch.int32, 2, device=dev)
     B, L = proposal.shape
+    if B * L != rows:
+        raise ValueError(f"proposal is [{B}, {L}], ver_hidden has {rows} rows")
+    _dev_tensor(cand_id, "cand_id", torch.int32, 2, device=dev)
     K = cand_id.shape[1]
-    d, V = ver_hidden.shape[1], lm_head.shape[0]
-    dev = ver_hidden.device
+    _dev_tensor(cand_id, "cand_id", torch.int32, shape=(rows, K), device=dev)
+    if cand_prob is not None:
+        _dev_tensor(cand_prob, "cand_prob", torch.float32, shape=(rows, K), device=dev)
+    _dev_tensor(u_accept, "u_accept", torch.float32, shape=(rows,), device=dev)
     nbytes = _sz(0)
     _check(lib().brisk_spec_verify_workspace_size(B, L, V, K, ctypes.byref(nbytes)),
            "brisk_spec_verify_workspace_size")
     ws = workspace if workspace is not None else _workspace(dev, nbytes.value, "spec")
+    ws_n = _ws_bytes(ws, dev, nbytes.value)
     out = {"accept_len": torch.empty(B, dtype=torch.int32, device=dev),
            "correction": torch.empty(B, dtype=torch.int32, device=dev),
            "row_accept": torch.empty(B * L, dtype=torch.int32, device=dev),
@@ -500,6 +554,6 @@ def spec_verify(ver_hidden: torch.Tensor, lm_head: torch.Tensor, proposal: torch
                                  _ptr(cand_prob), _ptr(u_accept), int(seed) & ((1 << 64) - 1),
                                  float(temperature), B, L, K, d, V, _ptr(out["accept_len"]),
                                  _ptr(out["correction"]), _ptr(out["row_accept"]),
-                                 _ptr(out["row_resample"]), _ptr(ws), ws.numel(), _stream_ptr(dev, stream))
+                                 _ptr(out["row_resample"]), _ptr(ws), ws_n, _stream_ptr(dev, stream))
     _check(st, "brisk_spec_verify")
     return out

@@ -193,8 +193,10 @@ int rerank_impl(const brisk_corrector* c, const uint16_t* hidden, const uint16_t
   st = rerank_shape_check(c, B, L, K);
   if (st != BRISK_OK) return st;
   if (d < 8 || d > kMaxD || V < K) return BRISK_ERR_SHAPE;
-  // the scan addresses one sequence's step vectors with 32-bit byte offsets
-  if (static_cast<uint64_t>(L) * (2 + 3 * static_cast<uint64_t>(K)) * c->d_state * 4 >= (uint64_t{1} << 31))
+  // the scan addresses one sequence's step vectors with 32-bit byte offsets;
+  // each vector is padded to at least 256 floats
+  const uint64_t vec = c->d_state <= 256 ? 256 : static_cast<uint64_t>(c->d_state);
+  if (static_cast<uint64_t>(L) * (2 + 3 * static_cast<uint64_t>(K)) * vec * 4 >= (uint64_t{1} << 31))
     return BRISK_ERR_UNSUPPORTED;
   if (d % 8 != 0 || !aligned16(hidden) || !aligned16(ctx_hidden) || !aligned16(lm_head) ||
       !aligned16(tok_embed) || !aligned4(anchor_tok) || !aligned4(cand_logit) ||

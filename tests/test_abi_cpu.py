@@ -262,3 +262,54 @@ def test_spec_verify_validation(kw, want):
                                        a["T"], a["B"], a["L"], a["K"], a["d"], a["V"], a["acc"], a["cor"],
                                        a["ra"], a["rr"], a["ws"], a["ws_bytes"], None)
     assert st == want
+
+
+@pytest.mark.parametrize("K,L,want", [(16, 41943, EWS), (16, 41944, EUNSUP)])
+def test_rerank_scan_offset_limit_uses_padded_vectors(K, L, want):
+    """With d_state = 32 each step vector is still padded to 256 floats, so one
+    sequence's step blocks take L*(2+3K)*256*4 bytes: 41943 positions at K = 16
+    fit below 2^31 (the call reaches the workspace check), 41944 do not."""
+    c = _corr(d_state=32, max_L=1 << 16)
+    assert _rerank(c, B=1, L=L, K=K) == want
+
+
+def _psi_cpu(d=64, ds=32, dh=16, dt=16, dp=4, df=4, rk=16, max_L=8, **override):
+    import torch
+    d_in = dh + dt + dp + df
+    shp = {"A_h": (ds, d), "A_e": (ds, d), "P_h": (dh, d), "P_e": (dt, d), "pos_emb": (max_L, dp),
+           "P_phi": (df, 5), "W_z": (ds, d_in), "W_h": (ds, d_in), "W_s": (rk, ds), "W_c": (rk, d),
+           "w_g": (ds + 5,)}
+    shp.update(override)
+    return {n: torch.zeros(s, dtype=torch.bfloat16) for n, s in shp.items()}
+
+
+@pytest.mark.parametrize("field,bad", [
+    ("A_e", (32, 72)), ("P_h", (16, 72)), ("P_e", (16, 8)), ("P_phi", (4, 6)), ("W_z", (32, 41)),
+    ("W_h", (31, 40)), ("W_s", (16, 33)), ("W_c", (16, 72)), ("w_g", (36,)),
+])
+def test_corrector_refuses_inconsistent_parameter_shapes(field, bad):
+    """Each psi tensor's shape follows from A_h [d_state, d] and the widths the
+    other tensors declare; a mismatch would make a kernel read past a buffer."""
+    with pytest.raises(ValueError, match="must have shape"):
+        brisk.Corrector(_psi_cpu(**{field: bad}), 0.0, 0.0)
+    with pytest.raises(ValueError, match="HIP device"):     # consistent shapes reach the device check
+        brisk.Corrector(_psi_cpu(), 0.0, 0.0)
+
+
+def test_binding_tensor_checks():
+    """The binding's buffer check reports dtype, exact shape and layout errors
+    before the device (the entry points' own uses run on the GPU)."""
+    import torch
+    chk = brisk._dev_tensor
+    with pytest.raises(ValueError, match="must have shape"):
+        chk(torch.zeros(2, 3, dtype=torch.int32), "x", torch.int32, shape=(2, 4))
+    with pytest.raises(TypeError, match="int32"):
+        chk(torch.zeros(2, 3, dtype=torch.int64), "x", torch.int32, shape=(2, 3))
+    with pytest.raises(ValueError, match="contiguous"):
+        chk(torch.zeros(3, 2, dtype=torch.int32).t(), "x", torch.int32, shape=(2, 3))
+    with pytest.raises(ValueError, match="HIP device"):
+        chk(torch.zeros(2, 3, dtype=torch.int32), "x", torch.int32, shape=(2, 3))
+    with pytest.raises(TypeError, match="Tensor"):
+        brisk._ws_bytes(bytearray(16), torch.device("cpu"), 0)
+    with pytest.raises(ValueError, match="HIP device"):
+        brisk._ws_bytes(torch.zeros(16, dtype=torch.uint8), torch.device("cpu"), 0)
