@@ -2,13 +2,25 @@
 """Benchmark of one BRISK-DLM decoding step on one MI355X.
 
 A step is the whole hot path over one block batch: brisk_propose_block (LM
-head + fused top-K) and brisk_rerank_verify (the prefix-conditioned corrector
-followed by greedy verification of its selections).  Inputs are synthetic, drawn once
-on the GPU and resident in HBM before timing starts.
+head + fused top-K, as its two launches) and brisk_rerank_verify (the
+prefix-conditioned corrector followed by greedy verification of its
+selections).  Inputs are synthetic, drawn once on the GPU and resident in HBM
+before timing starts.
 
-Prints one JSON line: block positions per second, the propose stage's
-achieved HBM bandwidth (or MFMA rate) against the MI355X peak, per-stage
-times, and the CPU oracle timed on the host on a bounded sample.
+The headline workload is the largest one (4096 rows: 256 blocks of 16
+positions, LLaDA-8B shape).  The other full-size workloads are measured in the
+same run and reported under ``configs``.  For every workload:
+
+* the step time is the median over the timed steps, with HIP events between
+  consecutive steps (eager launches on one stream), and the same again for a
+  hipGraph of the step replayed (the paper replays its head with CUDA Graphs);
+* the step roofline is T_roof / t_step, with T_roof = max(bytes / HBM peak,
+  flops / bf16 MFMA peak) of the whole step's algorithmic work;
+* the dominant kernel (the LM-head pass) is timed with HIP events around its
+  launch inside the timed steps, against its own algorithmic bytes or flops.
+
+Prints one JSON line; the CPU oracle is timed on the host on a bounded sample
+of the headline workload.
 """
 from __future__ import annotations
 
@@ -22,22 +34,20 @@ import time
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_PEAK_TFLOPS = 2516.6      # dense bf16 MFMA: 256 CU x 4096 flop/clk x 2.4 GHz
 METRIC = "block positions/sec (propose+rerank+verify) and % HBM/MFMA roofline"
-DEFAULT_WORKLOAD = "llada8b-b1-l32"
+DEFAULT_WORKLOAD = "llada8b-b256-l16"
+SUB_WORKLOADS = ("llada8b-b1-l32", "llada8b-b64-l32", "dream7b-b16-l32")
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
 
 def parse():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    # Eager launches are the default: on the decode shape a replayed hipGraph
-    # of the step measured slower (about 3%), on the 2048-row shape 1% faster.
-    ap.add_argument("--graph", dest="graph", action="store_true", default=False,
-                    help="time hipGraph replay of the step instead of eager launches")
-    ap.add_argument("--eager", dest="graph", action="store_false",
-                    help="time eager launches of the step on one stream (the default)")
+    ap.add_argument("--configs", default=",".join(SUB_WORKLOADS),
+                    help="comma-separated further workloads measured in the same run ('' for none)")
+    ap.add_argument("--no-graph", action="store_true", help="skip the hipGraph-replay timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the side timings of the verifier, profile, loss and sampling calls "
@@ -48,14 +58,277 @@ def parse():
     return ap.parse_args()
 
 
-def propose_cost(wl):
-    """Algorithmic bytes and flops of brisk_propose_block for one step."""
-    rows = wl.B * wl.L
-    bytes_ = 2 * wl.V * wl.d + 2 * rows * wl.d + rows * wl.K * 8
-    flops = 2 * rows * wl.d * wl.V
+# ----------------------------------------------------------------- work model
+def corrector_widths(wl):
+    """Corrector widths of a workload's state width r (head configuration
+    table ratios): d_state = r, projections and rank r/2, position and
+    feature widths r/8."""
+    r = wl.r
+    return dict(ds=r, dh=r // 2, dt=r // 2, dp=r // 8, df=r // 8, rk=r // 2)
+
+
+def step_work(wl):
+    """Algorithmic bytes and flops of one step (propose + rerank + verify).
+
+    Bytes: the LM head once, the hidden states, the context states, the
+    corrector's parameters, the K candidate rows of E_out and the previous
+    token's row of E per position, and the outputs.  Flops: the LM-head
+    product plus, per position, the corrector in its sequential form (the
+    hidden and previous-token projections, W_c on the K candidates, the
+    minGRU maps, W_s, the residual dots and the previous token's logit), plus
+    Init once per sequence."""
+    c = corrector_widths(wl)
+    rows, d, V, K, B = wl.B * wl.L, wl.d, wl.V, wl.K, wl.B
+    d_in = c["dh"] + c["dt"] + c["dp"] + c["df"]
+    n_psi = (2 * c["ds"] * d + c["dh"] * d + c["dt"] * d + wl.L * c["dp"] + c["df"] * 5
+             + 2 * c["ds"] * d_in + c["rk"] * c["ds"] + c["rk"] * d + c["ds"] + 5)
+    bytes_ = (2 * V * d + 2 * rows * d + 2 * B * d + 2 * n_psi + rows * (K + 1) * 2 * d
+              + rows * K * 8 + rows * 4 + B * 8)
+    per_pos = (2 * d * c["dh"] + 2 * d * c["dt"] + 2 * d * c["rk"] * K + 4 * c["ds"] * d_in
+               + 2 * c["rk"] * c["ds"] + 2 * c["rk"] * K + 2 * d)
+    flops = 2 * rows * d * V + rows * per_pos + B * 4 * d * c["ds"]
     return bytes_, flops
 
 
+def lmhead_work(wl):
+    """Algorithmic bytes and flops of the LM-head pass alone: both operands
+    read once; its keys leave through the workspace, not counted."""
+    rows = wl.B * wl.L
+    return 2 * wl.V * wl.d + 2 * rows * wl.d, 2 * rows * wl.d * wl.V
+
+
+def t_roof(bytes_, flops):
+    return max(bytes_ / (HBM_PEAK_GBS * 1e9), flops / (BF16_PEAK_TFLOPS * 1e12))
+
+
+def is_mfma_bound(bytes_, flops):
+    return flops / bytes_ > BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
+
+
+def kernel_roofline(b, f, t):
+    """Achieved rate of one launch of b bytes / f flops taking t seconds,
+    against the peak of the bound its intensity puts it under."""
+    if not is_mfma_bound(b, f):
+        a = b / t / 1e9
+        return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(a / HBM_PEAK_GBS, 4)}
+    a = f / t / 1e12
+    return {"bound": "mfma", "achieved": round(a, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(a / BF16_PEAK_TFLOPS, 4)}
+
+
+# ----------------------------------------------------------------- timing
+class Step:
+    """Device buffers and the launches of one step of a workload."""
+
+    def __init__(self, brisk, blk):
+        import torch
+
+        self.brisk, self.blk = brisk, blk
+        wl = self.wl = blk.wl
+        dev = blk.H.device
+        self.corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
+        rows, K = wl.B * wl.L, wl.K
+        self.cl = torch.empty(rows, K, dtype=torch.float32, device=dev)
+        self.ci = torch.empty(rows, K, dtype=torch.int32, device=dev)
+        self.sel = torch.empty(wl.B, wl.L, dtype=torch.int32, device=dev)
+        self.acc = torch.empty(wl.B, dtype=torch.int32, device=dev)
+        self.cor = torch.empty(wl.B, dtype=torch.int32, device=dev)
+        self.ws_p = torch.empty(brisk.propose_workspace_size(rows, wl.d, wl.V, K), dtype=torch.uint8, device=dev)
+        self.ws_r = torch.empty(brisk.rerank_workspace_size(self.corr, wl.B, wl.L, K), dtype=torch.uint8,
+                                device=dev)
+
+    def lmhead(self):
+        self.brisk.propose_lmhead(self.blk.H, self.blk.W, self.wl.K, self.ws_p)
+
+    def rest(self):
+        """The propose call's merge, then rerank + verify."""
+        b, wl = self.blk, self.wl
+        self.brisk.propose_merge(wl.B * wl.L, wl.V, wl.K, self.ws_p, self.cl, self.ci)
+        self.brisk.rerank_verify(self.corr, b.H, b.h_c, b.x0, b.W, b.E, self.cl, self.ci, b.verifier, wl.B, wl.L,
+                                 selected=self.sel, accept_len=self.acc, correction=self.cor, workspace=self.ws_r)
+
+    def step(self):
+        self.lmhead()
+        self.rest()
+
+
+def time_eager(st, steps):
+    """``steps`` eager steps back to back on one stream, with a HIP event at
+    the start of each step and one after its LM-head launch.  Returns the
+    per-step times, the LM-head launch times (both ms) and the total span."""
+    import torch
+
+    ev0 = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    ev1 = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        ev0[i].record()
+        st.lmhead()
+        ev1[i].record()
+        st.rest()
+    ev0[steps].record()
+    torch.cuda.synchronize()
+    per_step = [ev0[i].elapsed_time(ev0[i + 1]) for i in range(steps)]
+    lm = [ev0[i].elapsed_time(ev1[i]) for i in range(steps)]
+    return per_step, lm, ev0[0].elapsed_time(ev0[steps])
+
+
+def time_graph(st, steps, warmup):
+    """The step captured once in a hipGraph and replayed; HIP events between
+    replays.  Returns the per-replay times (ms)."""
+    import torch
+
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            st.step()
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        g.replay()
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    for i in range(steps):
+        ev[i].record()
+        g.replay()
+    ev[steps].record()
+    torch.cuda.synchronize()
+    out = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    del g
+    return out
+
+
+def measure(brisk, blk, steps, warmup, graph):
+    """Step times and rooflines of one workload."""
+    import torch
+
+    st = Step(brisk, blk)
+    wl = blk.wl
+    for _ in range(warmup):
+        st.step()
+    torch.cuda.synchronize()
+    per_step, lm, span = time_eager(st, steps)
+    rows = wl.B * wl.L
+    sb, sf = step_work(wl)
+    tr = t_roof(sb, sf)
+    t_step = statistics.median(per_step) * 1e-3
+    t_lm = statistics.median(lm) * 1e-3
+    lb, lf = lmhead_work(wl)
+    res = {
+        "B": wl.B, "L": wl.L, "rows": rows, "d": wl.d, "V": wl.V, "K": wl.K, "r": wl.r,
+        "ms_per_step": round(t_step * 1e3, 5),
+        "ms_per_step_mean": round(span / steps, 5),
+        "value": round(rows / t_step, 1),
+        "step_roofline": {"bound": "mfma" if is_mfma_bound(sb, sf) else "hbm",
+                          "bytes": sb, "flops": sf, "t_roof_us": round(tr * 1e6, 2),
+                          "t_step_us": round(t_step * 1e6, 2), "frac": round(tr / t_step, 4)},
+        "lmhead": dict(kernel_roofline(lb, lf, t_lm), launch_us=round(t_lm * 1e6, 2)),
+        "stages_ms": {"lmhead": round(t_lm * 1e3, 5),
+                      "merge+rerank+verify": round((t_step - t_lm) * 1e3, 5)},
+    }
+    if graph:
+        gt = time_graph(st, steps, warmup)
+        tg = statistics.median(gt) * 1e-3
+        res["graph_replay"] = {"ms_per_step": round(tg * 1e3, 5), "value": round(rows / tg, 1),
+                               "step_frac": round(tr / tg, 4)}
+    torch.cuda.synchronize()
+    res["accept_hist"] = torch.bincount(st.acc.long(), minlength=wl.L + 1).cpu().tolist()
+    return st, res
+
+
+# ----------------------------------------------------------------- side timings
+def _evented(fn, reps):
+    import torch
+
+    for _ in range(3):
+        fn()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def time_accept_profile(brisk, dev, M, n_blocks=1 << 20, reps=50):
+    """brisk_accept_profile over n_blocks accepted-prefix lengths (the
+    statistics that feed the position weights), timed with HIP events."""
+    import torch
+
+    g = torch.Generator(device=dev).manual_seed(0)
+    lens = torch.randint(0, M + 1, (n_blocks,), generator=g, device=dev, dtype=torch.int32)
+    us = _evented(lambda: brisk.accept_profile(lens, M), reps)
+    return {"n_blocks": n_blocks, "M": M, "us_per_call": round(us, 2),
+            "read_GB_per_s": round(4 * n_blocks / (us * 1e-6) / 1e9, 1)}
+
+
+def _noisy_rows(blk, seed):
+    import torch
+
+    g = torch.Generator(device=blk.H.device).manual_seed(seed)
+    noise = torch.randn(blk.H.shape, generator=g, device=blk.H.device, dtype=torch.float32)
+    return (blk.H.float() + 0.3 * noise).to(torch.bfloat16), g
+
+
+def time_fused_verify(brisk, blk, wl, reps=10):
+    """One LM-head pass over this block's proposal rows plus the previous
+    block's verifier rows (bf16 of the hidden states plus sigma-scaled noise),
+    against two separate passes, timed with HIP events."""
+    import torch
+
+    Hv, _ = _noisy_rows(blk, 1)
+    both = torch.cat([blk.H, Hv], dim=0).contiguous()
+    rows = wl.B * wl.L
+    out = {"rows": f"{rows} proposal + {rows} verifier"}
+    out["fused_us"] = round(_evented(lambda: brisk.propose_verify(both, blk.W, rows, wl.K), reps), 2)
+
+    def separate():
+        brisk.propose_block(blk.H, blk.W, wl.K)
+        brisk.propose_verify(Hv, blk.W, 0, wl.K)
+
+    out["separate_us"] = round(_evented(separate, reps), 2)
+    return out
+
+
+def time_corrector_loss(brisk, st, reps=50):
+    """brisk_corrector_loss on this step's candidates, refined logits and
+    accept lengths, with verifier rows = bf16(hidden + 0.3 noise)."""
+    blk, wl = st.blk, st.wl
+    rr = brisk.rerank(st.corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, st.cl, st.ci, wl.B, wl.L, want_scores=True)
+    Hv, _ = _noisy_rows(blk, 2)
+    us = _evented(lambda: brisk.corrector_loss(Hv, blk.W, st.ci, st.cl, rr["refined"], st.acc, wl.B, wl.L), reps)
+    return {"positions": wl.B * wl.L, "us_per_call": round(us, 2)}
+
+
+def time_spec_verify(brisk, st, reps=10):
+    """brisk_spec_verify on verifier rows bf16(hidden + 0.3 noise), proposals
+    drawn from the softmax of the candidate logits mixed with the uniform law
+    (weight 0.3), temperature 1, fresh seed per call."""
+    import torch
+
+    blk, wl = st.blk, st.wl
+    Hv, g = _noisy_rows(blk, 3)
+    prob = (0.7 * torch.softmax(st.cl.float(), dim=1) + 0.3 / wl.K).contiguous()
+    pick = torch.multinomial(prob, 1, generator=g).view(-1)
+    x = st.ci.gather(1, pick[:, None]).view(wl.B, wl.L).contiguous()
+    u = torch.rand(wl.B * wl.L, generator=g, device=blk.H.device)
+    calls = [0]
+    last = {}
+
+    def fn():
+        calls[0] += 1
+        last["out"] = brisk.spec_verify(Hv, blk.W, x, st.ci, prob, u, 1000 + calls[0], 1.0)
+
+    us = _evented(fn, reps)
+    return {"positions": wl.B * wl.L, "us_per_call": round(us, 2),
+            "mean_accept_len": round(last["out"]["accept_len"].float().mean().item(), 3)}
+
+
+# ----------------------------------------------------------------- CPU baseline
 def cpu_baseline(blk, budget_s):
     """The oracle, as is, on host cores, over a bounded sample of the same
     workload: whole sequences of the batch (all L positions, propose + rerank +
@@ -95,113 +368,7 @@ def cpu_baseline(blk, budget_s):
                       f"verify, {spent:.1f} s); float64 numpy, host has {os.cpu_count()} logical CPUs"}
 
 
-def time_accept_profile(brisk, dev, M, n_blocks=1 << 20, reps=50):
-    """brisk_accept_profile over n_blocks accepted-prefix lengths (the
-    statistics that feed the position weights), timed with HIP events."""
-    import torch
-
-    g = torch.Generator(device=dev).manual_seed(0)
-    lens = torch.randint(0, M + 1, (n_blocks,), generator=g, device=dev, dtype=torch.int32)
-    for _ in range(3):
-        brisk.accept_profile(lens, M)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        brisk.accept_profile(lens, M)
-    e1.record()
-    torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) * 1e3 / reps
-    return {"n_blocks": n_blocks, "M": M, "us_per_call": round(us, 2),
-            "read_GB_per_s": round(4 * n_blocks / (us * 1e-6) / 1e9, 1)}
-
-
-def time_fused_verify(brisk, blk, wl, reps=20):
-    """One LM-head pass over this block's proposal rows plus the previous
-    block's verifier rows (bf16 of the hidden states plus sigma-scaled noise),
-    against two separate passes, timed with HIP events."""
-    import torch
-
-    g = torch.Generator(device=blk.H.device).manual_seed(1)
-    noise = torch.randn(blk.H.shape, generator=g, device=blk.H.device, dtype=torch.float32)
-    Hv = (blk.H.float() + 0.3 * noise).to(torch.bfloat16)
-    both = torch.cat([blk.H, Hv], dim=0).contiguous()
-    rows = wl.B * wl.L
-
-    def fused():
-        brisk.propose_verify(both, blk.W, rows, wl.K)
-
-    def separate():
-        brisk.propose_block(blk.H, blk.W, wl.K)
-        brisk.propose_verify(Hv, blk.W, 0, wl.K)
-
-    out = {"rows": f"{rows} proposal + {rows} verifier"}
-    for name, fn in (("fused_us", fused), ("separate_us", separate)):
-        for _ in range(3):
-            fn()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(reps):
-            fn()
-        e1.record()
-        torch.cuda.synchronize()
-        out[name] = round(e0.elapsed_time(e1) * 1e3 / reps, 2)
-    return out
-
-
-def time_corrector_loss(brisk, blk, wl, corr, cl, ci, acc, reps=50):
-    """brisk_corrector_loss on this step's candidates, refined logits and
-    accept lengths, with verifier rows = bf16(hidden + 0.3 noise)."""
-    import torch
-
-    rr = brisk.rerank(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, wl.B, wl.L, want_scores=True)
-    g = torch.Generator(device=blk.H.device).manual_seed(2)
-    Hv = (blk.H.float() + 0.3 * torch.randn(blk.H.shape, generator=g, device=blk.H.device)).to(torch.bfloat16)
-    fn = lambda: brisk.corrector_loss(Hv, blk.W, ci, cl, rr["refined"], acc, wl.B, wl.L)
-    for _ in range(3):
-        fn()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        fn()
-    e1.record()
-    torch.cuda.synchronize()
-    return {"positions": wl.B * wl.L, "us_per_call": round(e0.elapsed_time(e1) * 1e3 / reps, 2)}
-
-
-def time_spec_verify(brisk, blk, wl, cl, ci, reps=20):
-    """brisk_spec_verify on verifier rows bf16(hidden + 0.3 noise), proposals
-    drawn from the softmax of the candidate logits mixed with the uniform law
-    (weight 0.3), temperature 1, fresh seed per call."""
-    import torch
-
-    g = torch.Generator(device=blk.H.device).manual_seed(3)
-    Hv = (blk.H.float() + 0.3 * torch.randn(blk.H.shape, generator=g, device=blk.H.device)).to(torch.bfloat16)
-    prob = (0.7 * torch.softmax(cl.float(), dim=1) + 0.3 / wl.K).contiguous()
-    pick = torch.multinomial(prob, 1, generator=g).view(-1)
-    x = ci.gather(1, pick[:, None]).view(wl.B, wl.L).contiguous()
-    u = torch.rand(wl.B * wl.L, generator=g, device=blk.H.device)
-    calls = [0]
-
-    def fn():
-        calls[0] += 1
-        return brisk.spec_verify(Hv, blk.W, x, ci, prob, u, 1000 + calls[0], 1.0)
-
-    for _ in range(3):
-        fn()
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for _ in range(reps):
-        out = fn()
-    e1.record()
-    torch.cuda.synchronize()
-    return {"positions": wl.B * wl.L, "us_per_call": round(e0.elapsed_time(e1) * 1e3 / reps, 2),
-            "mean_accept_len": round(out["accept_len"].float().mean().item(), 3)}
-
-
+# ----------------------------------------------------------------- counters
 def copy_calibration(n_bytes=1 << 30, reps=3):
     """A plain streaming kernel of known size (read n_bytes, write n_bytes),
     run so that HBM byte counters can be scaled against it."""
@@ -214,6 +381,16 @@ def copy_calibration(n_bytes=1 << 30, reps=3):
     torch.cuda.synchronize()
     print(json.dumps({"copy_calibration": {"kernel": "torch.neg (float32)", "read_bytes": n_bytes,
                                            "write_bytes": n_bytes, "launches": reps}}), flush=True)
+
+
+def kernel_source_hash():
+    import hashlib
+
+    h = hashlib.sha256()
+    for name in ("lmhead_topk.hip", "device_common.h"):
+        with open(os.path.join(ROOT, "paper_2609_33390_amd", "csrc", name), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 
 
 def counter_traffic(wl):
@@ -237,16 +414,7 @@ def counter_traffic(wl):
         return None
 
 
-def kernel_source_hash():
-    import hashlib
-
-    h = hashlib.sha256()
-    for name in ("lmhead_topk.hip", "device_common.h"):
-        with open(os.path.join(ROOT, "paper_2609_33390_amd", "csrc", name), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()
-
-
+# ----------------------------------------------------------------- main
 def main():
     args = parse()
     if args.gpus != 1:
@@ -262,153 +430,51 @@ def main():
     import paper_2609_33390_amd as brisk
     import synth
 
-    wl = synth.WORKLOADS[args.workload]
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    graph = not args.no_graph
+
+    subs = {}
+    for name in [n for n in args.configs.split(",") if n and n != args.workload]:
+        blk = synth.make_block(synth.WORKLOADS[name], dev)
+        _, r = measure(brisk, blk, args.steps, args.warmup, graph)
+        r["lmhead"]["traffic"] = counter_traffic(blk.wl)
+        subs[name] = r
+        print(f"# {name}: {r['ms_per_step']:.4f} ms/step, step roofline {r['step_roofline']['frac']}, "
+              f"LM-head {r['lmhead']['frac']} of {r['lmhead']['bound']}", file=sys.stderr, flush=True)
+        del blk, _
+        torch.cuda.empty_cache()
+
+    wl = synth.WORKLOADS[args.workload]
     blk = synth.make_block(wl, dev)
-    corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
-    rows, K = wl.B * wl.L, wl.K
-    cl = torch.empty(rows, K, dtype=torch.float32, device=dev)
-    ci = torch.empty(rows, K, dtype=torch.int32, device=dev)
-    sel = torch.empty(wl.B, wl.L, dtype=torch.int32, device=dev)
-    acc = torch.empty(wl.B, dtype=torch.int32, device=dev)
-    cor = torch.empty(wl.B, dtype=torch.int32, device=dev)
-    ws_p = torch.empty(brisk.propose_workspace_size(rows, wl.d, wl.V, K), dtype=torch.uint8, device=dev)
-    ws_r = torch.empty(brisk.rerank_workspace_size(corr, wl.B, wl.L, K), dtype=torch.uint8, device=dev)
+    st, head = measure(brisk, blk, args.steps, args.warmup, graph)
+    print(f"# {wl.name}: {head['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
 
-    # brisk_propose_block as its two launches, so that the LM-head pass (the
-    # dominant kernel) is timed on its own
-    def lmhead():
-        brisk.propose_lmhead(blk.H, blk.W, K, ws_p)
-
-    def merge():
-        brisk.propose_merge(rows, wl.V, K, ws_p, cl, ci)
-
-    def propose():
-        lmhead()
-        merge()
-
-    def rest():
-        brisk.rerank_verify(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl, ci, blk.verifier, wl.B, wl.L,
-                            selected=sel, accept_len=acc, correction=cor, workspace=ws_r)
-
-    for _ in range(args.warmup):
-        propose()
-        rest()
-    torch.cuda.synchronize()
-
-    n = args.steps
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(n)]
-    def eager_total():
-        """n eager steps back to back; returns their total time in ms."""
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t0.record()
-        for _ in range(n):
-            propose()
-            rest()
-        t1.record()
-        torch.cuda.synchronize()
-        return t0.elapsed_time(t1)
-
-    def eager_stages():
-        """n more eager steps with HIP events around each launch group (the
-        events themselves add stream work, so these steps are not the timed
-        ones); returns the per-step LM-head, propose and rerank+verify times."""
-        torch.cuda.synchronize()
-        for i in range(n):
-            ev[i][0].record()
-            lmhead()
-            ev[i][1].record()
-            merge()
-            ev[i][2].record()
-            rest()
-            ev[i][3].record()
-        torch.cuda.synchronize()
-        return ([ev[i][0].elapsed_time(ev[i][1]) for i in range(n)],
-                [ev[i][0].elapsed_time(ev[i][2]) for i in range(n)],
-                [ev[i][2].elapsed_time(ev[i][3]) for i in range(n)])
-
-    if args.graph:
-        # the whole step captured once and replayed: one launch per step
-        g = torch.cuda.CUDAGraph()
-        s = torch.cuda.Stream()
-        s.wait_stream(torch.cuda.current_stream())
-        with torch.cuda.stream(s):
-            with torch.cuda.graph(g, stream=s):
-                propose()
-                rest()
-        torch.cuda.synchronize()
-        for _ in range(args.warmup):
-            g.replay()
-        torch.cuda.synchronize()
-        t0 = torch.cuda.Event(enable_timing=True)
-        t1 = torch.cuda.Event(enable_timing=True)
-        t0.record()
-        for _ in range(n):
-            g.replay()
-        t1.record()
-        torch.cuda.synchronize()
-        total_ms = t0.elapsed_time(t1)
-        # per-launch figures (the roofline of the LM-head pass) from the same
-        # steps launched eagerly with events between them
-        lm_ms, prop_ms, rest_ms = eager_stages()
-    else:
-        total_ms = eager_total()
-        lm_ms, prop_ms, rest_ms = eager_stages()
-
-    ms_step = total_ms / n
-    value = rows / (ms_step * 1e-3)
-    bytes_, flops = propose_cost(wl)
-    t_lm = statistics.mean(lm_ms) * 1e-3
-    t_prop = statistics.mean(prop_ms) * 1e-3
-    ai = flops / bytes_
-    ridge = BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBS * 1e9)
-
-    def roofline(b, t):
-        if ai < ridge:
-            a = b / t / 1e9
-            return {"bound": "hbm", "achieved": round(a, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                    "frac": round(a / HBM_PEAK_GBS, 4)}
-        a = flops / t / 1e12
-        return {"bound": "mfma", "achieved": round(a, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(a / BF16_PEAK_TFLOPS, 4)}
-
-    # the dominant kernel: the LM-head pass (its candidates leave through the
-    # merge launch, so its algorithmic bytes are the two operands it reads)
-    roof = roofline(bytes_ - rows * wl.K * 8, t_lm)
+    roof = dict(head["lmhead"])
     roof["traffic"] = counter_traffic(wl)
     roof["kernel"] = "lmhead_topk_kernel (brisk_propose_lmhead, the LM-head pass of brisk_propose_block)"
-    roof["launch_us"] = round(t_lm * 1e6, 2)
-    call = roofline(bytes_, t_prop)
-    roof["propose_call"] = {"kernels": "lmhead_topk_kernel + topk_merge_kernel", "launch_us": round(t_prop * 1e6, 2),
-                            "achieved": call["achieved"], "frac": call["frac"]}
+    roof["step"] = head["step_roofline"]
 
-    torch.cuda.synchronize()
-    hist = torch.bincount(acc.long(), minlength=wl.L + 1).cpu().tolist()
-    if args.no_extras:
-        prof = fused = loss = spec = None
-    else:
-        prof = time_accept_profile(brisk, dev, wl.L)
-        fused = time_fused_verify(brisk, blk, wl)
-        loss = time_corrector_loss(brisk, blk, wl, corr, cl, ci, acc)
-        spec = time_spec_verify(brisk, blk, wl, cl, ci)
+    extras = {}
+    if not args.no_extras:
+        extras = {"accept_profile": time_accept_profile(brisk, dev, wl.L),
+                  "propose_verify": time_fused_verify(brisk, blk, wl),
+                  "corrector_loss": time_corrector_loss(brisk, st),
+                  "spec_verify": time_spec_verify(brisk, st)}
     res = {
-        "metric": METRIC, "value": round(value, 1), "unit": "block positions/s", "n_gpus": 1,
-        "steps": n, "warmup": args.warmup, "ms_per_step": round(ms_step, 5), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "metric": METRIC, "value": head["value"], "unit": "block positions/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": head["ms_per_step"],
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded; LLaDA/Dream-shaped random blocks, random-init corrector)",
-        "config": {"workload": wl.name, "B": wl.B, "L": wl.L, "d": wl.d, "V": wl.V, "K": wl.K,
-                   "r": wl.r, "timing": "hipGraph replay" if args.graph else "eager, one stream"},
+        "config": {"workload": wl.name, "B": wl.B, "L": wl.L, "d": wl.d, "V": wl.V, "K": wl.K, "r": wl.r,
+                   "timing": "eager, one stream; median of per-step HIP-event times"},
         "roofline": roof,
-        "stages_ms": {"lmhead": round(statistics.mean(lm_ms), 5), "propose": round(statistics.mean(prop_ms), 5),
-                      "rerank+verify": round(statistics.mean(rest_ms), 5)},
-        "accept_hist": hist,
-        "accept_profile": prof,
-        "propose_verify": fused,
-        "corrector_loss": loss,
-        "spec_verify": spec,
+        "ms_per_step_mean": head["ms_per_step_mean"],
+        "graph_replay": head.get("graph_replay"),
+        "stages_ms": head["stages_ms"],
+        "accept_hist": head["accept_hist"],
+        "configs": subs,
+        **extras,
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(blk, args.cpu_budget_s)
