@@ -16,9 +16,10 @@
  * Conventions shared by every entry point
  *   - Every pointer argument is a DEVICE pointer owned by the caller, except
  *     the brisk_corrector struct itself (host memory, read during the call)
- *     and the size out-parameters.  The library allocates nothing, keeps no
- *     global state and is reentrant; calls on different streams are safe when
- *     their workspaces and outputs differ.
+ *     and the size out-parameters.  The library allocates nothing and is
+ *     reentrant; calls on different streams are safe when their workspaces
+ *     and outputs differ.  Its only global state is the fixed scratch of
+ *     brisk_propose_block_noalloc (one array per GPU, and its address).
  *   - bf16 tensors are passed as uint16_t bit patterns; all matrices are
  *     row-major and densely packed (row stride = row length).
  *   - Rows of a block are numbered r = b * L + (i - 1) for sequence b and
@@ -50,7 +51,8 @@ typedef enum {
   BRISK_ERR_SHAPE = -2,       /* a size is out of range or inconsistent        */
   BRISK_ERR_UNSUPPORTED = -3, /* alignment / divisibility the kernels need     */
   BRISK_ERR_WORKSPACE = -4,   /* workspace missing or smaller than required    */
-  BRISK_ERR_HIP = -5          /* a HIP launch failed                           */
+  BRISK_ERR_HIP = -5,         /* a HIP launch failed                           */
+  BRISK_ERR_SCRATCH = -6      /* the shape needs more than the fixed scratch  */
 } brisk_status;
 
 /* Static, NUL-terminated description of a status code. */
@@ -120,6 +122,26 @@ int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head,
                         int32_t rows, int32_t d, int32_t V, int32_t K,
                         float* cand_logit, int32_t* cand_id,
                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * brisk_propose_block without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc).  Same arguments, results, limits and errors as
+ * brisk_propose_block, minus ws and ws_bytes: the key lists live in a fixed
+ * array of BRISK_NOALLOC_SCRATCH_BYTES (16 MiB) that the library holds on
+ * each GPU it runs on until the process ends.  A shape whose
+ * brisk_propose_workspace_size exceeds that returns BRISK_ERR_SCRATCH (the
+ * five decoding workloads need 0.5-8 MiB).  The call allocates nothing; its
+ * first call on a device looks up that device's copy of the array (with the
+ * stream's device made current for the lookup), and BRISK_ERR_HIP reports a
+ * failed lookup.  Every call on one GPU uses the same array: calls that
+ * overlap in time on one GPU (on different streams, or from different host
+ * threads) race and their results are undefined; serialise them.
+ */
+#define BRISK_NOALLOC_SCRATCH_BYTES ((size_t)16 << 20)
+int brisk_propose_block_noalloc(const uint16_t* hidden, const uint16_t* lm_head,
+                                int32_t rows, int32_t d, int32_t V, int32_t K,
+                                float* cand_logit, int32_t* cand_id, void* stream);
 
 /*
  * The two launches of brisk_propose_block, one call each (same section of the

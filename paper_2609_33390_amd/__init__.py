@@ -29,13 +29,14 @@ from typing import Dict, Optional, Tuple
 
 import torch
 
-__all__ = ["BriskError", "Corrector", "propose_block", "propose_lmhead", "propose_merge", "rerank", "rerank_verify", "verify_accept", "accept_profile",
+__all__ = ["BriskError", "Corrector", "propose_block", "propose_block_noalloc", "propose_lmhead", "propose_merge", "rerank", "rerank_verify", "verify_accept", "accept_profile",
            "propose_verify", "verify_commit", "corrector_loss", "spec_verify",
            "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libbrisk.so")
 ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace_size",
-               "brisk_propose_block", "brisk_propose_lmhead", "brisk_propose_merge",
+               "brisk_propose_block", "brisk_propose_block_noalloc", "brisk_propose_lmhead",
+               "brisk_propose_merge",
                "brisk_rerank_workspace_size", "brisk_rerank", "brisk_rerank_verify",
                "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
                "brisk_verify_commit", "brisk_spec_verify_workspace_size", "brisk_spec_verify",
@@ -83,6 +84,8 @@ def lib() -> ctypes.CDLL:
             L.brisk_propose_workspace_size.argtypes = [_i32, _i32, _i32, _i32, ctypes.POINTER(_sz)]
             L.brisk_propose_block.restype = ctypes.c_int
             L.brisk_propose_block.argtypes = [_p, _p, _i32, _i32, _i32, _i32, _p, _p, _p, _sz, _p]
+            L.brisk_propose_block_noalloc.restype = ctypes.c_int
+            L.brisk_propose_block_noalloc.argtypes = [_p, _p, _i32, _i32, _i32, _i32, _p, _p, _p]
             L.brisk_propose_lmhead.restype = ctypes.c_int
             L.brisk_propose_lmhead.argtypes = [_p, _p, _i32, _i32, _i32, _i32, _p, _sz, _p]
             L.brisk_propose_merge.restype = ctypes.c_int
@@ -238,6 +241,19 @@ def propose_block(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, *,
                                    _stream_ptr(dev, stream))
     _check(st, "brisk_propose_block")
     return cand_logit, cand_id
+
+
+def propose_block_noalloc(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, cand_logit: torch.Tensor,
+                          cand_id: torch.Tensor, *, stream=None) -> None:
+    """:func:`propose_block` on the library's fixed per-device scratch: the
+    library allocates nothing; the caller passes the [rows, K] outputs.  Calls
+    that overlap in time on one GPU race (they share the scratch)."""
+    rows, d, V, dev = _lmhead_operands(hidden, lm_head)
+    _dev_tensor(cand_logit, "cand_logit", torch.float32, shape=(rows, K), device=dev)
+    _dev_tensor(cand_id, "cand_id", torch.int32, shape=(rows, K), device=dev)
+    st = lib().brisk_propose_block_noalloc(_ptr(hidden), _ptr(lm_head), rows, d, V, K, _ptr(cand_logit),
+                                           _ptr(cand_id), _stream_ptr(dev, stream))
+    _check(st, "brisk_propose_block_noalloc")
 
 
 def propose_lmhead(hidden: torch.Tensor, lm_head: torch.Tensor, K: int, workspace: torch.Tensor, *,

@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 7;
+constexpr int kAbiVersion = 8;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 
@@ -83,6 +83,7 @@ const char* brisk_status_str(int status) {
     case BRISK_ERR_UNSUPPORTED: return "unsupported alignment or divisibility (16-byte pointers, d % 8 == 0)";
     case BRISK_ERR_WORKSPACE: return "workspace missing or too small";
     case BRISK_ERR_HIP: return "a HIP launch failed";
+    case BRISK_ERR_SCRATCH: return "the shape needs more scratch than the fixed no-alloc buffer holds";
     default: return "unknown status";
   }
 }
@@ -107,6 +108,17 @@ int brisk_propose_block(const uint16_t* hidden, const uint16_t* lm_head, int32_t
   if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
   brisk::launch_propose(hidden, lm_head, rows, d, V, K, rows, cand_logit, cand_id, nullptr, ws,
                         static_cast<hipStream_t>(stream));
+  return launch_status();
+}
+
+int brisk_propose_block_noalloc(const uint16_t* hidden, const uint16_t* lm_head, int32_t rows, int32_t d,
+                                int32_t V, int32_t K, float* cand_logit, int32_t* cand_id, void* stream) {
+  const int st = propose_check(hidden, lm_head, rows, d, V, K, cand_logit, cand_id);
+  if (st != BRISK_OK) return st;
+  if (brisk::propose_workspace_bytes(rows, V, K) > brisk::noalloc_scratch_bytes()) return BRISK_ERR_SCRATCH;
+  if (brisk::launch_propose_noalloc(hidden, lm_head, rows, d, V, K, cand_logit, cand_id,
+                                    static_cast<hipStream_t>(stream)) != 0)
+    return BRISK_ERR_HIP;
   return launch_status();
 }
 

@@ -23,6 +23,15 @@ void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V
                     int rows_prop, float* cand_logit, int32_t* cand_id, int32_t* ver_token,
                     void* ws, hipStream_t s);
 
+// The propose call on the library's fixed per-device scratch (the array
+// `scratch` in lmhead_topk.hip) instead of a caller's workspace; the caller
+// has checked that propose_workspace_bytes fits.  Returns 0, or -1 when the
+// stream's device or the scratch address cannot be determined (nothing is
+// launched then).
+size_t noalloc_scratch_bytes();
+int launch_propose_noalloc(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
+                           float* cand_logit, int32_t* cand_id, hipStream_t s);
+
 // ---- stochastic speculative verification ------------------------------------
 size_t spec_verify_workspace_bytes(int B, int L, int V, int K);
 void launch_spec_verify(const uint16_t* Hv, const uint16_t* W, int B, int L, int d, int V, int K,

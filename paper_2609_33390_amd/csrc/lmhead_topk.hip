@@ -18,8 +18,18 @@
 // slices in flight) and then meets the workgroup at a barrier.  Staged rows
 // are dense with their 16-byte chunks XOR-swizzled, which keeps the MFMA
 // operand reads (16 lanes, 16 rows, one chunk) free of bank conflicts.
+#include <mutex>
+
 #include "device_common.h"
 #include "kernels.h"
+
+// Fixed scratch of the propose call that allocates nothing
+// (brisk_propose_block_noalloc): the per-(row, vocabulary group) key lists
+// live here instead of in a caller's workspace.  Each GPU holds its own copy
+// for the life of the process; host code never uses this name as an address
+// (it is a host-side stand-in), only the device address that
+// hipGetSymbolAddress returns for it on each device.
+static __device__ __align__(256) unsigned char scratch[BRISK_NOALLOC_SCRATCH_BYTES];
 
 namespace brisk {
 
@@ -1060,6 +1070,51 @@ void launch_propose(const uint16_t* H, const uint16_t* W, int rows, int d, int V
                     void* ws, hipStream_t s) {
   launch_propose_pass(H, W, rows, d, V, K, ws, s);
   launch_propose_merge(rows, V, K, rows_prop, cand_logit, cand_id, ver_token, ws, s);
+}
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // device address of `scratch` on each device, once looked up
+
+// Device address of `scratch` on device `dev`, looked up on the first call
+// for that device with the device current (restored afterwards).
+void* scratch_on(int dev) {
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch[dev]) return g_scratch[dev];
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return nullptr;
+  if (cur != dev && hipSetDevice(dev) != hipSuccess) return nullptr;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (cur != dev) (void)hipSetDevice(cur);
+  if (e != hipSuccess || !p) return nullptr;
+  g_scratch[dev] = p;
+  return p;
+}
+
+}  // namespace
+
+size_t noalloc_scratch_bytes() { return BRISK_NOALLOC_SCRATCH_BYTES; }
+
+int launch_propose_noalloc(const uint16_t* H, const uint16_t* W, int rows, int d, int V, int K,
+                           float* cand_logit, int32_t* cand_id, hipStream_t s) {
+  int dev = -1;
+  if (s) {
+    hipDevice_t sd;
+    if (hipStreamGetDevice(s, &sd) != hipSuccess) return -1;
+    dev = static_cast<int>(sd);
+  } else if (hipGetDevice(&dev) != hipSuccess) {
+    return -1;
+  }
+  if (dev < 0 || dev >= kMaxDevices) return -1;
+  void* ws = scratch_on(dev);
+  if (!ws) return -1;
+  // every (row, group) list is written by the pass before the merge reads
+  // it, so nothing left by an earlier call needs clearing
+  launch_propose(H, W, rows, d, V, K, rows, cand_logit, cand_id, nullptr, ws, s);
+  return 0;
 }
 
 }  // namespace brisk

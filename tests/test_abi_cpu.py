@@ -38,8 +38,9 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 7
-    for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5):
+    assert L.brisk_abi_version() == 8
+    for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5, -6):
+        assert L.brisk_status_str(st).decode() != "unknown status"
         assert L.brisk_status_str(st).decode()
     assert L.brisk_status_str(123).decode() == "unknown status"
 
@@ -313,3 +314,32 @@ def test_binding_tensor_checks():
         brisk._ws_bytes(bytearray(16), torch.device("cpu"), 0)
     with pytest.raises(ValueError, match="HIP device"):
         brisk._ws_bytes(torch.zeros(16, dtype=torch.uint8), torch.device("cpu"), 0)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(hidden=None), ENULL), (dict(cl=None), ENULL), (dict(rows=0), ESHAPE), (dict(K=65), ESHAPE),
+    (dict(d=4092), EUNSUP), (dict(hidden=MISALIGNED), EUNSUP),
+    # 64 rows with 64-key lists: 1024 parts of 64 keys per row, 32 MiB > the 16 MiB scratch
+    (dict(rows=64, K=64), -6),
+])
+def test_propose_noalloc_validation(kw, want):
+    """Every rejection happens on the host before any HIP call, the scratch
+    limit included (the call never looks the scratch up for such a shape)."""
+    a = dict(hidden=FAKE, lm_head=FAKE, rows=32, d=4096, V=126464, K=8, cl=FAKE, ci=FAKE)
+    a.update(kw)
+    need = ctypes.c_size_t()
+    if want == -6:
+        assert brisk.lib().brisk_propose_workspace_size(a["rows"], a["d"], a["V"], a["K"],
+                                                        ctypes.byref(need)) == OK
+        assert need.value > (16 << 20)
+    assert brisk.lib().brisk_propose_block_noalloc(a["hidden"], a["lm_head"], a["rows"], a["d"], a["V"], a["K"],
+                                                   a["cl"], a["ci"], None) == want
+
+
+def test_noalloc_scratch_covers_the_decoding_workloads():
+    """The five decoding workloads fit the fixed scratch of the no-alloc call."""
+    import synth
+    out = ctypes.c_size_t()
+    for wl in synth.WORKLOADS.values():
+        assert brisk.lib().brisk_propose_workspace_size(wl.B * wl.L, wl.d, wl.V, wl.K, ctypes.byref(out)) == OK
+        assert out.value <= (16 << 20), wl.name
