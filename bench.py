@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--configs", default=",".join(SUB_WORKLOADS),
                     help="comma-separated further workloads measured in the same run ('' for none)")
     ap.add_argument("--no-graph", action="store_true", help="skip the hipGraph-replay timing")
+    ap.add_argument("--no-tables", action="store_true",
+                    help="rerank without the corrector's per-token tables (project the candidates' "
+                         "embedding rows in every step)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the side timings of the verifier, profile, loss and sampling calls "
@@ -119,15 +122,26 @@ def kernel_roofline(b, f, t):
 
 # ----------------------------------------------------------------- timing
 class Step:
-    """Device buffers and the launches of one step of a workload."""
+    """Device buffers and the launches of one step of a workload.  With
+    ``tables``, the corrector's per-token tables are prepared once here (a
+    per-model preparation, like loading the weights) and the timed steps read
+    them."""
 
-    def __init__(self, brisk, blk):
+    def __init__(self, brisk, blk, tables=True):
         import torch
 
         self.brisk, self.blk = brisk, blk
         wl = self.wl = blk.wl
         dev = blk.H.device
         self.corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
+        self.prepare_ms = None
+        if tables:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            self.corr.prepare(blk.W, blk.E)
+            e1.record()
+            torch.cuda.synchronize()
+            self.prepare_ms = round(e0.elapsed_time(e1), 3)
         rows, K = wl.B * wl.L, wl.K
         self.cl = torch.empty(rows, K, dtype=torch.float32, device=dev)
         self.ci = torch.empty(rows, K, dtype=torch.int32, device=dev)
@@ -200,11 +214,11 @@ def time_graph(st, steps, warmup):
     return out
 
 
-def measure(brisk, blk, steps, warmup, graph):
+def measure(brisk, blk, steps, warmup, graph, tables=True):
     """Step times and rooflines of one workload."""
     import torch
 
-    st = Step(brisk, blk)
+    st = Step(brisk, blk, tables)
     wl = blk.wl
     for _ in range(warmup):
         st.step()
@@ -227,6 +241,8 @@ def measure(brisk, blk, steps, warmup, graph):
         "lmhead": dict(kernel_roofline(lb, lf, t_lm), launch_us=round(t_lm * 1e6, 2)),
         "stages_ms": {"lmhead": round(t_lm * 1e3, 5),
                       "merge+rerank+verify": round((t_step - t_lm) * 1e3, 5)},
+        "corrector_tables": ({"prepare_ms": st.prepare_ms, "note": "once per model, outside the timed steps"}
+                             if st.prepare_ms is not None else None),
     }
     if graph:
         gt = time_graph(st, steps, warmup)
@@ -437,7 +453,7 @@ def main():
     subs = {}
     for name in [n for n in args.configs.split(",") if n and n != args.workload]:
         blk = synth.make_block(synth.WORKLOADS[name], dev)
-        _, r = measure(brisk, blk, args.steps, args.warmup, graph)
+        _, r = measure(brisk, blk, args.steps, args.warmup, graph, not args.no_tables)
         r["lmhead"]["traffic"] = counter_traffic(blk.wl)
         subs[name] = r
         print(f"# {name}: {r['ms_per_step']:.4f} ms/step, step roofline {r['step_roofline']['frac']}, "
@@ -447,7 +463,7 @@ def main():
 
     wl = synth.WORKLOADS[args.workload]
     blk = synth.make_block(wl, dev)
-    st, head = measure(brisk, blk, args.steps, args.warmup, graph)
+    st, head = measure(brisk, blk, args.steps, args.warmup, graph, not args.no_tables)
     print(f"# {wl.name}: {head['ms_per_step']:.4f} ms/step", file=sys.stderr, flush=True)
 
     roof = dict(head["lmhead"])
@@ -472,6 +488,7 @@ def main():
         "ms_per_step_mean": head["ms_per_step_mean"],
         "graph_replay": head.get("graph_replay"),
         "stages_ms": head["stages_ms"],
+        "corrector_tables": head["corrector_tables"],
         "accept_hist": head["accept_hist"],
         "configs": subs,
         **extras,

@@ -93,7 +93,41 @@ typedef struct brisk_corrector {
   const uint16_t* w_g;      /* [d_state + 5]                              */
   float alpha;              /* gate scale logit (host value)               */
   float b_g;                /* gate bias (host value)                      */
+  /* Optional per-token tables from brisk_corrector_prepare (NULL: none).
+   * When set, the rerank calls read the lifts of candidate and anchor tokens
+   * from them instead of projecting their embedding rows; tables_V must then
+   * equal the call's V, and the tables must have been prepared from these
+   * parameters and the same lm_head and tok_embed (not checked). */
+  const float* tables;      /* [3][tables_V][max(256, d_state)] fp32       */
+  int32_t tables_V;
 } brisk_corrector;
+
+/*
+ * Per-token tables of the corrector (Section 3.3 Eq. inference_head_state and
+ * Eq. candidate_residual; Appendix Eq. head_residual_logits).  Every map the
+ * corrector applies to a token's embedding rows is linear and fixed once the
+ * model is loaded: the token projection reaches the state update as
+ * TZ(v) = W_z[:, t] P_e E(v) and TH(v) = W_h[:, t] P_e E(v), and the residual
+ * re-associates to <u_i, EH(v)> with EH(v) = W_s^T W_c E_out(v) (t = the
+ * d_tproj columns of W_z and W_h that read P_e E).  brisk_corrector_prepare
+ * computes the three for every token (bf16 inputs, fp32 accumulation) into
+ * tables [EH; TZ; TH], each [V][max(256, d_state)] fp32 with rows zero-padded
+ * past d_state.  Preparing once per model replaces the per-step gathers of
+ * whole E and E_out rows by gathers of table rows; the decoding results are
+ * those of the per-step projections up to fp32 rounding.
+ *
+ *   c          corrector parameters (its tables field is ignored here)
+ *   lm_head    [V, d] bf16  E_out;   tok_embed [V, d] bf16  E
+ *   tables     out, table_bytes >= *table_bytes of brisk_corrector_tables_size
+ *   ws         scratch of at least *ws_bytes bytes (V * (d_tproj + rank) fp32)
+ *
+ * Limits as brisk_rerank's for the corrector; 1 <= V <= 2^24, 8 <= d <= 65536,
+ * d % 8 == 0, 16-byte aligned pointers.
+ */
+int brisk_corrector_tables_size(const brisk_corrector* c, int32_t V, size_t* table_bytes, size_t* ws_bytes);
+int brisk_corrector_prepare(const brisk_corrector* c, const uint16_t* lm_head, const uint16_t* tok_embed,
+                            int32_t V, int32_t d, float* tables, size_t table_bytes, void* ws,
+                            size_t ws_bytes, void* stream);
 
 /*
  * Workspace bytes brisk_propose_block needs for this shape (written to *bytes).

@@ -41,7 +41,7 @@ ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace
                "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
                "brisk_verify_commit", "brisk_spec_verify_workspace_size", "brisk_spec_verify",
                "brisk_corrector_loss", "brisk_accept_profile_workspace_size",
-               "brisk_accept_profile")
+               "brisk_accept_profile", "brisk_corrector_tables_size", "brisk_corrector_prepare")
 PSI_FIELDS = ("A_h", "A_e", "P_h", "P_e", "pos_emb", "P_phi", "W_z", "W_h", "W_s", "W_c", "w_g")
 
 _p = ctypes.c_void_p
@@ -60,7 +60,7 @@ class BriskError(RuntimeError):
 class _CorrectorC(ctypes.Structure):
     _fields_ = ([(n, _i32) for n in ("d_state", "d_hproj", "d_tproj", "d_pos", "d_feat", "rank", "max_L")]
                 + [(n, _p) for n in PSI_FIELDS]
-                + [("alpha", ctypes.c_float), ("b_g", ctypes.c_float)])
+                + [("alpha", ctypes.c_float), ("b_g", ctypes.c_float), ("tables", _p), ("tables_V", _i32)])
 
 
 _lib = None
@@ -123,6 +123,12 @@ def lib() -> ctypes.CDLL:
             L.brisk_accept_profile.restype = ctypes.c_int
             L.brisk_accept_profile.argtypes = [_p, _i32, _i32, ctypes.c_double, _p, _p, _p, _p, _p,
                                                _sz, _p]
+            L.brisk_corrector_tables_size.restype = ctypes.c_int
+            L.brisk_corrector_tables_size.argtypes = [ctypes.POINTER(_CorrectorC), _i32, ctypes.POINTER(_sz),
+                                                      ctypes.POINTER(_sz)]
+            L.brisk_corrector_prepare.restype = ctypes.c_int
+            L.brisk_corrector_prepare.argtypes = [ctypes.POINTER(_CorrectorC), _p, _p, _i32, _i32, _p, _sz, _p,
+                                                  _sz, _p]
             _lib = L
         return _lib
 
@@ -310,11 +316,43 @@ class Corrector:
         for n in PSI_FIELDS:
             _dev_tensor(t[n], n, torch.bfloat16, shape=want[n], device=self.device)
         self._c = _CorrectorC(**self.dims, **{n: _ptr(self.t[n]) for n in PSI_FIELDS},
-                              alpha=self.alpha, b_g=self.b_g)
+                              alpha=self.alpha, b_g=self.b_g, tables=None, tables_V=0)
+        self.tables: Optional[torch.Tensor] = None
 
     @property
     def c_struct(self) -> _CorrectorC:
         return self._c
+
+    def prepare(self, lm_head: torch.Tensor, tok_embed: torch.Tensor, *, stream=None) -> torch.Tensor:
+        """Compute the per-token tables (brisk_corrector_prepare) for this LM
+        head and input embedding; later rerank calls read the candidates' and
+        anchors' lifts from them.  Returns the [3, V, max(256, d_state)] fp32
+        tables, which the corrector keeps."""
+        _dev_tensor(lm_head, "lm_head", torch.bfloat16, 2, device=self.device)
+        V, d = lm_head.shape
+        if d != self.d:
+            raise ValueError(f"lm_head has d = {d}, the corrector d = {self.d}")
+        _dev_tensor(tok_embed, "tok_embed", torch.bfloat16, shape=(V, d), device=self.device)
+        tb, wb = _sz(), _sz()
+        _check(lib().brisk_corrector_tables_size(ctypes.byref(self._c), V, ctypes.byref(tb), ctypes.byref(wb)),
+               "brisk_corrector_tables_size")
+        vs = max(256, self.dims["d_state"])
+        tables = torch.empty(3, V, vs, dtype=torch.float32, device=self.device)
+        ws = torch.empty(wb.value, dtype=torch.uint8, device=self.device)
+        _check(lib().brisk_corrector_prepare(ctypes.byref(self._c), _ptr(lm_head), _ptr(tok_embed), V, d,
+                                             _ptr(tables), tables.numel() * 4, _ptr(ws), wb.value,
+                                             _stream_ptr(self.device, stream)),
+               "brisk_corrector_prepare")
+        self.tables = tables
+        self._c.tables = _ptr(tables)
+        self._c.tables_V = V
+        return tables
+
+    def drop_tables(self) -> None:
+        """Forget the per-token tables: rerank projects the embedding rows again."""
+        self.tables = None
+        self._c.tables = None
+        self._c.tables_V = 0
 
 
 def rerank_workspace_size(corr: Corrector, B: int, L: int, K: int) -> int:

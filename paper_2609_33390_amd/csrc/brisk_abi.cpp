@@ -10,9 +10,10 @@
 
 namespace {
 
-constexpr int kAbiVersion = 8;
+constexpr int kAbiVersion = 9;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
+constexpr int32_t kMaxTableV = 1 << 24;
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
@@ -215,6 +216,8 @@ int rerank_impl(const brisk_corrector* c, const uint16_t* hidden, const uint16_t
       !aligned4(cand_id) || !aligned4(selected) || !aligned4(refined) || !aligned4(gamma) ||
       !aligned4(resid))
     return BRISK_ERR_UNSUPPORTED;
+  if (c->tables && (c->tables_V != V)) return BRISK_ERR_SHAPE;
+  if (!aligned16(c->tables)) return BRISK_ERR_UNSUPPORTED;
   const size_t need = brisk::rerank_workspace_bytes(*c, B, L, K);
   if (ws_bytes < need || !ws) return BRISK_ERR_WORKSPACE;
   if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
@@ -247,6 +250,31 @@ int brisk_rerank_verify(const brisk_corrector* c, const uint16_t* hidden, const 
   return rerank_impl(c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
                      verifier, B, L, K, d, V, selected, refined, gamma, resid, accept_len, correction,
                      ws, ws_bytes, stream);
+}
+
+int brisk_corrector_tables_size(const brisk_corrector* c, int32_t V, size_t* table_bytes, size_t* ws_bytes) {
+  if (!table_bytes || !ws_bytes) return BRISK_ERR_NULL;
+  const int st = corrector_check(c);
+  if (st != BRISK_OK) return st;
+  if (V < 1 || V > kMaxTableV) return BRISK_ERR_SHAPE;
+  *table_bytes = brisk::corrector_tables_bytes(*c, V);
+  *ws_bytes = brisk::corrector_prepare_ws_bytes(*c, V);
+  return BRISK_OK;
+}
+
+int brisk_corrector_prepare(const brisk_corrector* c, const uint16_t* lm_head, const uint16_t* tok_embed,
+                            int32_t V, int32_t d, float* tables, size_t table_bytes, void* ws,
+                            size_t ws_bytes, void* stream) {
+  int st = corrector_check(c);
+  if (st != BRISK_OK) return st;
+  if (!lm_head || !tok_embed || !tables) return BRISK_ERR_NULL;
+  if (V < 1 || V > kMaxTableV || d < 8 || d > kMaxD) return BRISK_ERR_SHAPE;
+  if (d % 8 != 0 || !aligned16(lm_head) || !aligned16(tok_embed) || !aligned16(tables)) return BRISK_ERR_UNSUPPORTED;
+  if (table_bytes < brisk::corrector_tables_bytes(*c, V)) return BRISK_ERR_WORKSPACE;
+  if (ws_bytes < brisk::corrector_prepare_ws_bytes(*c, V) || !ws) return BRISK_ERR_WORKSPACE;
+  if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
+  brisk::launch_corrector_prepare(*c, lm_head, tok_embed, V, d, tables, ws, static_cast<hipStream_t>(stream));
+  return launch_status();
 }
 
 int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_t B, int32_t L,

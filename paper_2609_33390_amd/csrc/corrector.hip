@@ -1134,6 +1134,51 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Step blocks from the per-token tables (brisk_corrector_prepare): for row r
+// and candidate k the vectors EH_k, TZ_k, TH_k are rows c_{r,k} of the EH, TZ
+// and TH tables, and the anchor lifts TZA, THA are rows x_0 of TZ and TH.
+// One wavefront copies one vector, 16 bytes per lane.
+// ---------------------------------------------------------------------------
+struct FillArgs {
+  const float* tables;   // [3][V][vs]: EH, TZ, TH
+  const int32_t* cand_id;
+  const int32_t* anchor;
+  float* SB;             // [rows][2 + 3K][vs]
+  float* TZA;            // [B][ds]
+  float* THA;
+  int rows, K, B, V, ds, vs;
+};
+
+__global__ __launch_bounds__(256) void fill_kernel(FillArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int n_cand = a.rows * 3 * a.K;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= n_cand + 2 * a.B) return;
+  const float* src;
+  float* dst;
+  int len;
+  if (n < n_cand) {
+    const int r = n / (3 * a.K), f = n % (3 * a.K), kind = f / a.K, k = f % a.K;
+    const int v = clamp_id(a.cand_id[static_cast<size_t>(r) * a.K + k], a.V);
+    src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
+    dst = a.SB + (static_cast<size_t>(r) * (2 + 3 * a.K) + 2 + f) * a.vs;
+    len = a.vs;
+  } else {
+    const int m = n - n_cand, b = m % a.B, kind = 1 + m / a.B;  // TZ, then TH
+    const int v = clamp_id(a.anchor[b], a.V);
+    src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
+    dst = (kind == 1 ? a.TZA : a.THA) + static_cast<size_t>(b) * a.ds;
+    len = a.ds;
+  }
+  if ((len & 3) == 0) {
+    for (int e = lane * 4; e < len; e += 256)
+      *reinterpret_cast<float4*>(dst + e) = *reinterpret_cast<const float4*>(src + e);
+  } else {
+    for (int e = lane; e < len; e += 64) dst[e] = src[e];
+  }
+}
+
 // Vector stride of the step blocks: one 256-float vector per field when the
 // state fits (the single-wave scan copies whole 1 KiB vectors), else d_state.
 size_t step_vec_stride(int ds) { return ds <= 256 ? 256 : static_cast<size_t>(ds); }
@@ -1217,12 +1262,16 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   // Slices of PE are [NP, d_tproj]: candidate rows, then anchor rows.
   // Slices of U0 are [2, B, ds]: A_h h_c, then A_e E(x_0).
   const size_t sPE = lay.sPE, sPC = lay.sPC, sPH = lay.sPH, sU0 = lay.sU0;
+  // With the per-token tables, every per-candidate and per-anchor lift is a
+  // table row: the projections of candidates and anchors are not computed.
+  const bool tab = c.tables != nullptr;
+  const int n_cand = tab ? 0 : NC, n_anch = tab ? 0 : B;
   ProjJobs pj{};
   pj.d = d;
   pj.splits = S;
-  pj.job[0] = ProjJob{tok_embed, cand_id, NC, c.d_tproj, V, c.P_e, F(lay.PE), sPE};
-  pj.job[1] = ProjJob{tok_embed, anchor_tok, B, c.d_tproj, V, c.P_e, F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj, sPE};
-  pj.job[2] = ProjJob{lm_head, cand_id, NC, c.rank, V, c.W_c, F(lay.PC), sPC};
+  pj.job[0] = ProjJob{tok_embed, cand_id, n_cand, c.d_tproj, V, c.P_e, F(lay.PE), sPE};
+  pj.job[1] = ProjJob{tok_embed, anchor_tok, n_anch, c.d_tproj, V, c.P_e, F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj, sPE};
+  pj.job[2] = ProjJob{lm_head, cand_id, n_cand, c.rank, V, c.W_c, F(lay.PC), sPC};
   pj.job[3] = ProjJob{hidden, nullptr, rows, c.d_hproj, rows, c.P_h, F(lay.PH), sPH};
   pj.job[4] = ProjJob{ctx_hidden, nullptr, B, ds, B, c.A_h, F(lay.U0), sU0};
   pj.job[5] = ProjJob{tok_embed, anchor_tok, B, ds, V, c.A_e, F(lay.U0) + static_cast<size_t>(B) * ds, sU0};
@@ -1246,8 +1295,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   if (S > 1) {
     SliceArrs sl{};
     sl.splits = S;
-    sl.arr[0] = SliceArr{F(lay.PE), sPE, sPE};
-    sl.arr[1] = SliceArr{F(lay.PC), sPC, sPC};
+    sl.arr[0] = SliceArr{F(lay.PE), tab ? 0 : sPE, sPE};
+    sl.arr[1] = SliceArr{F(lay.PC), tab ? 0 : sPC, sPC};
     sl.arr[2] = SliceArr{F(lay.PH), sPH, sPH};
     sl.arr[3] = SliceArr{F(lay.U0), sU0, sU0};
     size_t mx = sPE > sPC ? sPE : sPC;
@@ -1285,23 +1334,30 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   const LiftTerm posz = term(c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1);
   const LiftTerm posh = term(c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1);
   const size_t vds = static_cast<size_t>(ds);
-  lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, NC, SB + (2 + K) * vsz, K, blk, vsz};
-  lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, NC, SB + (2 + 2 * K) * vsz, K, blk, vsz};
-  lj.job[2] = LiftJob{{fterm(F(lay.PC), c.rank, c.W_s, 1, ds), none}, NC, SB + 2 * vsz, K, blk, vsz};
+  lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, n_cand, SB + (2 + K) * vsz, K, blk, vsz};
+  lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, n_cand, SB + (2 + 2 * K) * vsz, K, blk, vsz};
+  lj.job[2] = LiftJob{{fterm(F(lay.PC), c.rank, c.W_s, 1, ds), none}, n_cand, SB + 2 * vsz, K, blk, vsz};
   lj.job[3] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_z, d_in, 1), posz}, rows, SB, 1, blk, vsz};
   lj.job[4] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_h, d_in, 1), posh}, rows, SB + vsz, 1, blk, vsz};
-  lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, B, F(lay.TZA), 1, vds, vds};
-  lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, B, F(lay.THA), 1, vds, vds};
+  lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, n_anch, F(lay.TZA), 1, vds, vds};
+  lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, n_anch, F(lay.THA), 1, vds, vds};
   // feature maps W_z[:, feat] P_phi and W_h[:, feat] P_phi as [5, ds]: input row f is column f of P_phi
   lj.job[7] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1), none}, 5, F(lay.FZ), 1, vds, vds};
   lj.job[8] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1), none}, 5, F(lay.FH), 1, vds, vds};
   const int lift_cols = static_cast<int>(vsz > vds ? vsz : vds);
-  const int lift_rows = NC > 2 * B ? NC : 2 * B;
+  int lift_rows = 0;
+  for (int j = 0; j < kMaxLiftJobs; ++j) lift_rows = lj.job[j].n > lift_rows ? lj.job[j].n : lift_rows;
   const dim3 lift_grid((lift_rows + LT_BN - 1) / LT_BN, (lift_cols + LT_BJ - 1) / LT_BJ, kMaxLiftJobs);
   // the candidate jobs' tiles: more than two per compute unit -> one buffer
-  const bool many_tiles = 3 * ((NC + LT_BN - 1) / LT_BN) * ((ds + LT_BJ - 1) / LT_BJ) > 512;
+  const bool many_tiles = 3 * ((n_cand + LT_BN - 1) / LT_BN) * ((ds + LT_BJ - 1) / LT_BJ) > 512;
   if (many_tiles) hipLaunchKernelGGL(lift_kernel<1>, lift_grid, dim3(256), 0, s, lj);
   else hipLaunchKernelGGL(lift_kernel<2>, lift_grid, dim3(256), 0, s, lj);
+  if (tab) {
+    const FillArgs fa{c.tables, cand_id, anchor_tok, SB, F(lay.TZA), F(lay.THA), rows, K, B, V, ds,
+                      static_cast<int>(vsz)};
+    const int n_vec = rows * 3 * K + 2 * B;
+    hipLaunchKernelGGL(fill_kernel, dim3((n_vec + 3) / 4), dim3(256), 0, s, fa);
+  }
 
   ScanArgs sa{};
   sa.B = B; sa.L = L; sa.K = K; sa.ds = ds; sa.vs = static_cast<int>(vsz);
@@ -1326,6 +1382,52 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   else if (K <= 16) launch_scan<16, 3>(sa, B, nw, s);
   else launch_scan<64, 1>(sa, B, nw, s);
   if (verifier && !pc) launch_verify(selected, verifier, B, L, accept_len, correction, s);
+}
+
+size_t corrector_tables_bytes(const brisk_corrector& c, int V) {
+  return 3 * static_cast<size_t>(V) * step_vec_stride(c.d_state) * sizeof(float);
+}
+
+size_t corrector_prepare_ws_bytes(const brisk_corrector& c, int V) {
+  return static_cast<size_t>(V) * (c.d_tproj + c.rank) * sizeof(float);
+}
+
+// The per-token tables: P_e E(v) and W_c E_out(v) for every token (the
+// gathered projections with the identity as row map), then their lifts
+// TZ = W_z[:, t] P_e E(v), TH = W_h[:, t] P_e E(v) and EH = W_s^T W_c E_out(v),
+// each row zero-padded to the step-vector stride.
+void launch_corrector_prepare(const brisk_corrector& c, const uint16_t* lm_head, const uint16_t* tok_embed,
+                              int V, int d, float* tables, void* ws, hipStream_t s) {
+  const int ds = c.d_state;
+  const int d_in = c.d_hproj + c.d_tproj + c.d_pos + c.d_feat;
+  const int tp_off = c.d_hproj;
+  const size_t vsz = step_vec_stride(ds);
+  float* PE = static_cast<float*>(ws);
+  float* PC = PE + static_cast<size_t>(V) * c.d_tproj;
+  ProjJobs pj{};
+  pj.d = d;
+  pj.splits = 1;
+  pj.job[0] = ProjJob{tok_embed, nullptr, V, c.d_tproj, V, c.P_e, PE, static_cast<size_t>(V) * c.d_tproj};
+  pj.job[2] = ProjJob{lm_head, nullptr, V, c.rank, V, c.W_c, PC, static_cast<size_t>(V) * c.rank};
+  int gx = 0;
+  for (int j = 0; j < kMaxProjJobs; ++j) gx = std::max(gx, proj_tiles(pj.job[j].n, pj.job[j].J, 128));
+  hipLaunchKernelGGL(gather_proj_kernel<128>, dim3(gx, kMaxProjJobs + 1, 1), dim3(256), 0, s, pj);
+
+  auto fterm = [&](const float* in, int C, const uint16_t* m, int m_rs, int m_cs) {
+    const bool a16 = (reinterpret_cast<uintptr_t>(in) & 15u) == 0 && C % 16 == 0;
+    const bool m16 = (reinterpret_cast<uintptr_t>(m) & 15u) == 0 &&
+                     (m_cs == 1 ? m_rs % 8 == 0 && C % 16 == 0 : m_rs == 1 && m_cs % 8 == 0 && ds % 16 == 0);
+    return LiftTerm{in, 0, C, 1, 0, C, m, m_rs, m_cs, a16 ? 1 : 0, m16 ? 1 : 0};
+  };
+  const LiftTerm none{nullptr, 0, 0, 0, 0, 0, nullptr, 0, 0, 0, 0};
+  const size_t tstride = static_cast<size_t>(V) * vsz;
+  LiftJobs lj{};
+  lj.ds = ds;
+  lj.job[0] = LiftJob{{fterm(PC, c.rank, c.W_s, 1, ds), none}, V, tables, 1, vsz, vsz};
+  lj.job[1] = LiftJob{{fterm(PE, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, V, tables + tstride, 1, vsz, vsz};
+  lj.job[2] = LiftJob{{fterm(PE, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, V, tables + 2 * tstride, 1, vsz, vsz};
+  const dim3 grid((V + LT_BN - 1) / LT_BN, static_cast<int>((vsz + LT_BJ - 1) / LT_BJ), kMaxLiftJobs);
+  hipLaunchKernelGGL(lift_kernel<1>, grid, dim3(256), 0, s, lj);
 }
 
 }  // namespace brisk

@@ -49,6 +49,13 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
                    const int32_t* verifier, int32_t* accept_len, int32_t* correction, void* ws,
                    hipStream_t s);
 
+// Per-token tables [EH; TZ; TH], each [V][step vector stride] fp32, and the
+// scratch their preparation needs.
+size_t corrector_tables_bytes(const brisk_corrector& c, int V);
+size_t corrector_prepare_ws_bytes(const brisk_corrector& c, int V);
+void launch_corrector_prepare(const brisk_corrector& c, const uint16_t* lm_head, const uint16_t* tok_embed,
+                              int V, int d, float* tables, void* ws, hipStream_t s);
+
 // ---- verify -----------------------------------------------------------------
 void launch_verify(const int32_t* proposal, const int32_t* verifier, int B, int L,
                    int32_t* accept_len, int32_t* correction, hipStream_t s);

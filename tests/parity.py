@@ -46,11 +46,14 @@ def check_candidates(cl, ci, ol, tol=SCORE_TOL):
                 assert ci[r, k] == order[r, k], (r, k)
 
 
-def check_rerank(gpu, orc, tol=SCORE_TOL):
+def check_rerank(gpu, orc, tol=SCORE_TOL, rel=0.0):
     """Conditional check: ``orc`` is the oracle run on the GPU's candidates with
-    the GPU's selected prefix forced."""
-    r_err = np.max(np.abs(gpu["refined"] - orc["refined"]))
-    assert r_err <= tol, (r_err, np.max(np.abs(orc["refined"])))
+    the GPU's selected prefix forced.  ``rel`` adds a relative part to the
+    score bound: tol + rel * |gamma * d| per score (for corrector weights far
+    beyond the workloads', where fp32 cannot reach the absolute bound)."""
+    allowed = tol + rel * np.abs(orc["gamma"][:, None].astype(np.float64) * orc["resid"])
+    r_err = np.abs(gpu["refined"].astype(np.float64) - orc["refined"])
+    assert np.all(r_err <= allowed), (r_err.max(), np.max(np.abs(orc["refined"])))
     g_err = np.abs(gpu["gamma"].astype(np.float64) - orc["gamma"])
     assert np.all(g_err <= 1e-3 * np.abs(orc["gamma"]) + 1e-6), g_err.max()
     dmax = np.max(np.abs(orc["resid"]), axis=1, keepdims=True)
@@ -58,17 +61,19 @@ def check_rerank(gpu, orc, tol=SCORE_TOL):
     assert np.all(d_err <= 1e-3 * dmax + 1e-6), d_err.max()
     sel_g = gpu["selected"].ravel()
     sel_o = orc["selected"].ravel()
-    sure = orc["margin"] > tol
+    sure = orc["margin"] > np.max(allowed, axis=1)
     assert np.array_equal(sel_g[sure], sel_o[sure])
     # near-ties: the GPU's pick scores within tol of the oracle's best
     return int((~sure).sum())
 
 
-def rerank_pick_ok(gpu_sel, orc, cand_id, tol=SCORE_TOL):
-    """Every GPU pick is a candidate whose oracle refined score is within tol of the best."""
+def rerank_pick_ok(gpu_sel, orc, cand_id, tol=SCORE_TOL, rel=0.0):
+    """Every GPU pick is a candidate whose oracle refined score is within the
+    score bound (tol, plus rel * max |gamma * d| of the row) of the best."""
     rows, K = cand_id.shape
     sel = gpu_sel.ravel()
+    slack = tol + rel * np.max(np.abs(orc["gamma"][:, None].astype(np.float64) * orc["resid"]), axis=1)
     for r in range(rows):
         k = np.nonzero(cand_id[r] == sel[r])[0]
         assert k.size == 1, r
-        assert orc["refined"][r, k[0]] >= orc["refined"][r].max() - tol, r
+        assert orc["refined"][r, k[0]] >= orc["refined"][r].max() - slack[r], r

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 8
+    assert L.brisk_abi_version() == 9
     for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5, -6):
         assert L.brisk_status_str(st).decode() != "unknown status"
         assert L.brisk_status_str(st).decode()
@@ -343,3 +343,37 @@ def test_noalloc_scratch_covers_the_decoding_workloads():
     for wl in synth.WORKLOADS.values():
         assert brisk.lib().brisk_propose_workspace_size(wl.B * wl.L, wl.d, wl.V, wl.K, ctypes.byref(out)) == OK
         assert out.value <= (16 << 20), wl.name
+
+
+def test_corrector_tables_size_and_prepare_validation():
+    """The per-token tables: sizes, and every rejection before any HIP call."""
+    L = brisk.lib()
+    c = _corr()
+    tb, wb = ctypes.c_size_t(), ctypes.c_size_t()
+    assert L.brisk_corrector_tables_size(ctypes.byref(c), 126464, ctypes.byref(tb), ctypes.byref(wb)) == OK
+    assert tb.value == 3 * 126464 * 256 * 4                   # [EH; TZ; TH], rows of 256 floats
+    assert wb.value == 126464 * (128 + 128) * 4               # P_e E and W_c E_out for every token
+    assert L.brisk_corrector_tables_size(ctypes.byref(c), 0, ctypes.byref(tb), ctypes.byref(wb)) == ESHAPE
+    assert L.brisk_corrector_tables_size(ctypes.byref(c), 10, None, ctypes.byref(wb)) == ENULL
+    big = _corr(d_state=320)
+    assert L.brisk_corrector_tables_size(ctypes.byref(big), 10, ctypes.byref(tb), ctypes.byref(wb)) == OK
+    assert tb.value == 3 * 10 * 320 * 4                       # rows of d_state floats beyond 256
+
+    def prep(**kw):
+        a = dict(W=FAKE, E=FAKE, V=1000, d=4096, tab=FAKE, tab_bytes=1 << 40, ws=FAKE, ws_bytes=1 << 40)
+        a.update(kw)
+        return L.brisk_corrector_prepare(ctypes.byref(c), a["W"], a["E"], a["V"], a["d"], a["tab"],
+                                         a["tab_bytes"], a["ws"], a["ws_bytes"], None)
+    assert prep(W=None) == ENULL and prep(tab=None) == ENULL
+    assert prep(V=0) == ESHAPE and prep(d=4) == ESHAPE
+    assert prep(d=4092) == EUNSUP and prep(tab=MISALIGNED) == EUNSUP
+    assert prep(tab_bytes=16) == EWS and prep(ws_bytes=16) == EWS and prep(ws=None) == EWS
+
+
+def test_rerank_refuses_tables_of_another_vocabulary():
+    c = _corr(tables=FAKE, tables_V=1000)
+    assert _rerank(c, V=126464) == ESHAPE
+    c = _corr(tables=MISALIGNED, tables_V=126464)
+    assert _rerank(c, V=126464) == EUNSUP
+    c = _corr(tables=FAKE, tables_V=126464)
+    assert _rerank(c, V=126464) == EWS                        # passes the table checks

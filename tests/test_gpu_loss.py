@@ -39,7 +39,8 @@ def _check(g, o):
     assert g["loss_mean"][0] == pytest.approx(o["mean"], rel=1e-3, abs=1e-3)
 
 
-@pytest.mark.parametrize("name", ["tiny-d64-v512", "llada8b-b1-l32"])
+@pytest.mark.parametrize("name", ["tiny-d64-v512", "llada8b-b1-l32",
+                                  pytest.param("llada8b-b64-l32", marks=pytest.mark.slow)])
 def test_loss_matches_oracle(name):
     _check(*_run(synth.WORKLOADS[name]))
 

@@ -62,6 +62,32 @@ def test_fused_pass_matches_separate_pass_and_oracle(wl_name, sample):
     _say(f"  [{wl_name}] near-tie verifier rows: {near}")
 
 
+@pytest.mark.slow
+def test_fused_pass_batched_shape():
+    """The fused pass at the shape the benchmark times for the 2048-row
+    workload: 2048 proposal rows and 2048 verifier rows in one launch (16 row
+    tiles of the large-row tile).  Checked on the first and last row of every
+    256-row tile of both halves, plus random rows."""
+    wl = synth.WORKLOADS["llada8b-b64-l32"]
+    blk = synth.make_block(wl, "cuda")
+    Hv = _verifier_rows(blk, 0.3, 11)
+    hidden = torch.cat([blk.H, Hv], dim=0).contiguous()
+    rows = wl.rows
+    cl, ci, vt = brisk.propose_verify(hidden, blk.W, rows, wl.K)
+    cl_s, ci_s = brisk.propose_block(blk.H, blk.W, wl.K)
+    torch.cuda.synchronize()
+    assert torch.equal(ci, ci_s) and torch.equal(cl, cl_s)
+    rng = np.random.default_rng(5)
+    edges = sorted({t for t0 in range(0, rows, 256) for t in (t0, t0 + 255)})
+    rs = np.array(sorted(set(edges) | set(rng.choice(rows, 32, replace=False).tolist())))
+    W_bits, Hv_bits, H_bits = synth.bf16_bits(blk.W), synth.bf16_bits(Hv), synth.bf16_bits(blk.H)
+    _say(f"  oracle on {len(rs)} proposal and {len(rs)} verifier rows")
+    near = _check_argmax(vt.cpu().numpy(), Hv_bits, W_bits, rs)
+    ol = oracle.lm_logits(oracle.bf16_to_f64(H_bits[rs]), W_bits)
+    check_candidates(cl.cpu().numpy()[rs], ci.cpu().numpy()[rs], ol)
+    _say(f"  near-tie verifier rows: {near}")
+
+
 # (100, 300, 16): 400 rows on the large-row tile with 16-key lists, whose
 # epilogue filters survivors
 @pytest.mark.parametrize("rows_prop,rows_ver,K", [(0, 40, 5), (40, 0, 5), (1, 1, 5), (100, 300, 5),
