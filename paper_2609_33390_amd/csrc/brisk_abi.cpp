@@ -217,6 +217,8 @@ int rerank_impl(const brisk_corrector* c, const uint16_t* hidden, const uint16_t
       !aligned4(resid))
     return BRISK_ERR_UNSUPPORTED;
   if (c->tables && (c->tables_V != V)) return BRISK_ERR_SHAPE;
+  // the scan addresses the tables with 32-bit byte offsets
+  if (c->tables && 3 * static_cast<uint64_t>(V) * vec * 4 >= (uint64_t{1} << 31)) return BRISK_ERR_UNSUPPORTED;
   if (!aligned16(c->tables)) return BRISK_ERR_UNSUPPORTED;
   const size_t need = brisk::rerank_workspace_bytes(*c, B, L, K);
   if (ws_bytes < need || !ws) return BRISK_ERR_WORKSPACE;

@@ -599,6 +599,11 @@ struct ScanArgs {
   const int32_t* verifier;
   int32_t* accept_len;
   int32_t* correction;
+  // optional per-token tables [EH; TZ; TH] (single-wave scan only): the
+  // candidates' and the anchor's vectors are read from them by token id,
+  // and the step blocks hold only AZ and AH
+  const float* tables;
+  int V;
 };
 
 template <int KM>
@@ -841,8 +846,11 @@ __device__ __forceinline__ float sigmoid_rcp(float x) {
   return __builtin_amdgcn_rcpf(1.0f + __expf(-x));
 }
 
-template <int KM, int D>
-__global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
+// `ids` is the candidate-id array again, as a kernel argument of its own: read
+// only and unaliased, so the copy engine's wave-uniform reads of it become
+// scalar loads, which leave the vector-memory counter to the row copies.
+template <int KM, int D, bool TAB>
+__global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a, const int32_t* __restrict__ ids_in) {
   using S = LdsStage<KM>;
   static_assert((D - 2) * S::NDMA <= 63, "vmcnt range");
   static_assert(2 * KM <= 62, "output lanes");
@@ -864,6 +872,25 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
         const_cast<int32_t*>(a.cand_id + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
     const __amdgpu_buffer_rsrc_t rxs = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<float*>(a.X + row0 * K), static_cast<short>(0), L * K * 4, 0x00020000);
+    // the tables' byte size fits 32 bits (checked on the host)
+    constexpr bool tab = TAB;
+    const __amdgpu_buffer_rsrc_t rtb = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(tab ? a.tables : a.SB), static_cast<short>(0),
+        tab ? static_cast<int>(3u * static_cast<unsigned>(a.V) * 1024u) : 0, 0x00020000);
+    // Token ids of the candidates of row i, wave-uniform (scalar loads),
+    // fetched one row before the row's copies are issued.
+    int ids[KM];
+    auto load_ids = [&](int i) {
+      const int ii = i < L ? i : L - 1;
+      const int32_t* src = ids_in + (row0 + ii) * K;
+      // all loads first, one wait for them
+#pragma unroll
+      for (int k = 0; k < KM; ++k) ids[k] = src[k < K ? k : K - 1];
+    };
+    auto clamp_ids = [&] {
+#pragma unroll
+      for (int k = 0; k < KM; ++k) ids[k] = __builtin_amdgcn_readfirstlane(clamp_id(ids[k], a.V));
+    };
     // Copies of row i (clamped to the block) into slot i % D.  Candidate slots
     // k >= K repeat candidate K-1, so every row issues exactly NDMA copies and
     // vmcnt(n * NDMA) always means "every row but the n last issued landed".
@@ -871,8 +898,17 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
       const int ii = i < L ? i : L - 1;
       float* st = ring + (i % D) * S::FLOATS;
       const unsigned rb = static_cast<unsigned>(ii * F) * 1024u;
+      if constexpr (tab) clamp_ids();
 #pragma unroll
       for (int v = 0; v < S::NVEC; ++v) {
+        if (tab && v >= 2) {
+          // table kind (EH, TZ, TH) and candidate slot of vector v
+          const int kind = (v - 2) / KM, k = (v - 2) % KM;
+          const unsigned off = (static_cast<unsigned>(kind) * static_cast<unsigned>(a.V) +
+                                static_cast<unsigned>(ids[k])) * 1024u;
+          __builtin_amdgcn_raw_ptr_buffer_load_lds(rtb, (lds_vptr_t)(st + v * 256), 16, lane * 16, off, 0, 0);
+          continue;
+        }
         int f;
         if (v < 2) f = v;
         else if (v < 2 + KM) f = 2 + min(v - 2, K - 1);
@@ -925,7 +961,11 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
     // LDS writes complete before the barrier that hands the row over
     auto handover = [] { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); };
 #pragma unroll
-    for (int t = 0; t < D - 1; ++t) issue(t);
+    for (int t = 0; t < D - 1; ++t) {
+      if constexpr (tab) load_ids(t);
+      issue(t);
+    }
+    if constexpr (tab) load_ids(D - 1);
     wait_vm<(D - 2) * S::NDMA>();  // row 0 has landed
     prep(0);
     for (int i = 0; i < L; ++i) {
@@ -933,6 +973,7 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
       prep(i + 1);
       handover();                    // hand slot i over; slot (i-1) % D is free again
       issue(i + D - 1);
+      if constexpr (tab) load_ids(i + D);  // the next row's ids, used at the next step
     }
     wait_vm<0>();  // no copy may land after the workgroup's LDS is released
     return;
@@ -949,7 +990,15 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a) {
     const float u0b = a.U0[static_cast<size_t>(a.B + b) * ds + e];
     u[j] = ok ? tanhf(u0a + u0b) : 0.f;
     wgu[j] = ok ? bf16_to_f32(a.w_g[e]) : 0.f;
-    const float tz = a.TZA[static_cast<size_t>(b) * ds + e], th = a.THA[static_cast<size_t>(b) * ds + e];
+    float tz, th;
+    if constexpr (TAB) {  // the anchor's rows of the TZ and TH tables
+      const size_t x0 = static_cast<size_t>(clamp_id(a.anchor[b], a.V));
+      tz = a.tables[(static_cast<size_t>(a.V) + x0) * 256 + e];
+      th = a.tables[(2 * static_cast<size_t>(a.V) + x0) * 256 + e];
+    } else {
+      tz = a.TZA[static_cast<size_t>(b) * ds + e];
+      th = a.THA[static_cast<size_t>(b) * ds + e];
+    }
     ptz[j] = ok ? tz : 0.f;
     pth[j] = ok ? th : 0.f;
 #pragma unroll
@@ -1352,7 +1401,18 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   const bool many_tiles = 3 * ((n_cand + LT_BN - 1) / LT_BN) * ((ds + LT_BJ - 1) / LT_BJ) > 512;
   if (many_tiles) hipLaunchKernelGGL(lift_kernel<1>, lift_grid, dim3(256), 0, s, lj);
   else hipLaunchKernelGGL(lift_kernel<2>, lift_grid, dim3(256), 0, s, lj);
-  if (tab) {
+  const bool pc = ds <= 256 && K <= 16;  // the single-wave scan, which can verify in the same pass
+  // Who brings the table rows to the scan.  The single-wave scan can gather
+  // them itself (its copy wave issues each row's copies three rows ahead), but
+  // random 1 KiB reads from the tables outlast that lead: at 32 rows the scan
+  // took 40 instead of 23 us, with 16 keys (two rows of lead) 72 instead of
+  // 36 us.  Copying the rows into the step blocks first is a parallel,
+  // bandwidth-bound pass (5 us at 32 rows, 32 us at 4096); it loses only when
+  // there are many short sequences (4096 rows as 256 x 16: 165 against
+  // 140 us for the whole rerank), where the gathering scan is used.
+  const bool scan_gathers = tab && pc && K <= 8 && B >= 128;
+  if (tab && !scan_gathers) {
+    // the scan reads whole step blocks: copy the table rows in
     const FillArgs fa{c.tables, cand_id, anchor_tok, SB, F(lay.TZA), F(lay.THA), rows, K, B, V, ds,
                       static_cast<int>(vsz)};
     const int n_vec = rows * 3 * K + 2 * B;
@@ -1367,17 +1427,22 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   sa.cand_logit = cand_logit; sa.cand_id = cand_id; sa.anchor = anchor_tok;
   sa.selected = selected; sa.refined = refined; sa.gamma = gamma; sa.resid = resid;
   sa.dump = F(lay.DUMP);
-  const bool pc = ds <= 256 && K <= 16;  // the single-wave scan, which can verify in the same pass
+  if (scan_gathers) {  // the single-wave scan gathers the table rows itself
+    sa.tables = c.tables;
+    sa.V = V;
+  }
   if (verifier && pc) {
     sa.verifier = verifier;
     sa.accept_len = accept_len;
     sa.correction = correction;
   }
   const int nw = (ds + 63) / 64;
-  if (ds <= 256 && K <= 8)
-    hipLaunchKernelGGL((scan_pc_kernel<8, 4>), dim3(B), dim3(128), 0, s, sa);
+  if (scan_gathers)
+    hipLaunchKernelGGL((scan_pc_kernel<8, 4, true>), dim3(B), dim3(128), 0, s, sa, cand_id);
+  else if (ds <= 256 && K <= 8)
+    hipLaunchKernelGGL((scan_pc_kernel<8, 4, false>), dim3(B), dim3(128), 0, s, sa, cand_id);
   else if (ds <= 256 && K <= 16)
-    hipLaunchKernelGGL((scan_pc_kernel<16, 3>), dim3(B), dim3(128), 0, s, sa);
+    hipLaunchKernelGGL((scan_pc_kernel<16, 3, false>), dim3(B), dim3(128), 0, s, sa, cand_id);
   else if (K <= 8) launch_scan<8, 4>(sa, B, nw, s);
   else if (K <= 16) launch_scan<16, 3>(sa, B, nw, s);
   else launch_scan<64, 1>(sa, B, nw, s);

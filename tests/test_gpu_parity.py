@@ -294,7 +294,10 @@ REL_GATE = 2e-5
     # about 70 and the absolute bound holds; at std 0.3 they reach about 4.4e3
     # and the bound gains its relative part (REL_GATE).
     (70, 30, 8, 72, 700, 96, 0.3, 0.0), (30, 40, 16, 136, 900, 320, 0.1, 0.0),
-    (30, 40, 16, 136, 900, 320, 0.3, REL_GATE)])
+    (30, 40, 16, 136, 900, 320, 0.3, REL_GATE),
+    # 130 sequences with K <= 8: with the tables, the single-wave scan gathers
+    # the table rows itself instead of reading copied step blocks
+    (130, 5, 6, 72, 900, 96, 0.3, 0.0)])
 def test_rerank_ragged(B, L, K, d, V, r, psi, rel, tables):
     wl = synth.Workload("ragged", B=B, L=L, d=d, V=V, K=K, r=r, sigma=0.3, flat_frac=0.5, seed=B + L + K)
     blk = synth.make_block(wl, "cpu", psi_std=psi)
