@@ -49,6 +49,7 @@ struct CrossJob {
   const int32_t* anchor;
   int B, L, K, V;
   float* X;
+  int group;  // candidates per wavefront, 1..8
 };
 struct ProjJobs {
   ProjJob job[kMaxProjJobs];
@@ -68,48 +69,79 @@ constexpr int PJ_NPB = PJ_BN * PJ_CPR / 256;  // gathered-row pieces per thread
 static_assert(PJ_NPB >= 1 && PJ_BN * PJ_CPR % 256 == 0, "staging map");
 constexpr int PJ_PF = 2;  // reduction chunks in flight per thread
 
-// One wavefront per cross logit, eight 16-byte loads of each operand in
-// flight per lane.
+// One wavefront per row and group of up to `group` of its candidates: the
+// hidden row m_{r+1} is read once for all of them, two 512-element chunks of
+// every operand in flight per lane.  Anchors take one wavefront each.  Groups
+// of eight when there are many dots (the hidden row is re-read less); one
+// candidate per wavefront when there are few, which keeps more wavefronts
+// in flight (32 rows: 257 wavefronts instead of 33).
+__device__ __forceinline__ float dot8_bf16(uint4 a, uint4 c, float s) {
+  s += bf16_lo(a.x) * bf16_lo(c.x) + bf16_hi(a.x) * bf16_hi(c.x);
+  s += bf16_lo(a.y) * bf16_lo(c.y) + bf16_hi(a.y) * bf16_hi(c.y);
+  s += bf16_lo(a.z) * bf16_lo(c.z) + bf16_hi(a.z) * bf16_hi(c.z);
+  s += bf16_lo(a.w) * bf16_lo(c.w) + bf16_hi(a.w) * bf16_hi(c.w);
+  return s;
+}
+
 __device__ void cross_dots(const CrossJob& cj, int d) {
+  constexpr int G = 8, U = 2;
   const int lane = threadIdx.x & 63;
-  const int NC = cj.B * cj.L * cj.K;
+  const int rows = cj.B * cj.L, NC = rows * cj.K;
+  const int g = cj.group;
+  const int nkb = (cj.K + g - 1) / g;
+  const int items = rows * nkb + cj.B;
   const int waves = gridDim.x * gridDim.z * 4;
-  for (int n = (blockIdx.z * gridDim.x + blockIdx.x) * 4 + (threadIdx.x >> 6); n < NC + cj.B; n += waves) {
-    int v, hrow;
-    if (n < NC) {
-      const int r = n / cj.K;
-      if (r % cj.L == cj.L - 1) {
-        if (lane == 0) cj.X[n] = 0.f;
+  for (int it = (blockIdx.z * gridDim.x + blockIdx.x) * 4 + (threadIdx.x >> 6); it < items; it += waves) {
+    int hrow, nk;
+    float* xo;
+    const uint16_t* w[G];
+    if (it < rows * nkb) {
+      const int r = it / nkb, k0 = (it % nkb) * g;
+      nk = min(g, cj.K - k0);
+      xo = cj.X + static_cast<size_t>(r) * cj.K + k0;
+      if (r % cj.L == cj.L - 1) {  // the last row of a block has no next row
+        if (lane < nk) xo[lane] = 0.f;
         continue;
       }
-      v = clamp_id(cj.cand_id[n], cj.V);
       hrow = r + 1;
+#pragma unroll
+      for (int q = 0; q < G; ++q) {
+        const int v = clamp_id(cj.cand_id[static_cast<size_t>(r) * cj.K + k0 + min(q, nk - 1)], cj.V);
+        w[q] = cj.W + static_cast<size_t>(v) * d;
+      }
     } else {
-      const int b = n - NC;
-      v = clamp_id(cj.anchor[b], cj.V);
+      const int b = it - rows * nkb;
+      nk = 1;
+      xo = cj.X + NC + b;
       hrow = b * cj.L;
+      const int v = clamp_id(cj.anchor[b], cj.V);
+#pragma unroll
+      for (int q = 0; q < G; ++q) w[q] = cj.W + static_cast<size_t>(v) * d;
     }
-    const uint16_t* w = cj.W + static_cast<size_t>(v) * d;
     const uint16_t* h = cj.H + static_cast<size_t>(hrow) * d;
-    float s = 0.f;
-    for (int k0 = lane * 8; k0 < d; k0 += 8 * 512) {
-      uint4 a[8], c[8];
+    float acc[G];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+    for (int q = 0; q < G; ++q) acc[q] = 0.f;
+    for (int k0 = lane * 8; k0 < d; k0 += 512 * U) {
+      uint4 hv[U], wv[G][U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
         const int k = k0 + u * 512;
-        a[u] = k < d ? *reinterpret_cast<const uint4*>(w + k) : make_uint4(0, 0, 0, 0);
-        c[u] = k < d ? *reinterpret_cast<const uint4*>(h + k) : make_uint4(0, 0, 0, 0);
+        hv[u] = k < d ? *reinterpret_cast<const uint4*>(h + k) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < G; ++q)
+          wv[q][u] = k < d && q < nk ? *reinterpret_cast<const uint4*>(w[q] + k) : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        s += bf16_lo(a[u].x) * bf16_lo(c[u].x) + bf16_hi(a[u].x) * bf16_hi(c[u].x);
-        s += bf16_lo(a[u].y) * bf16_lo(c[u].y) + bf16_hi(a[u].y) * bf16_hi(c[u].y);
-        s += bf16_lo(a[u].z) * bf16_lo(c[u].z) + bf16_hi(a[u].z) * bf16_hi(c[u].z);
-        s += bf16_lo(a[u].w) * bf16_lo(c[u].w) + bf16_hi(a[u].w) * bf16_hi(c[u].w);
-      }
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int q = 0; q < G; ++q) acc[q] = dot8_bf16(wv[q][u], hv[u], acc[q]);
     }
-    s = wave_sum(s);
-    if (lane == 0) cj.X[n] = s;
+#pragma unroll
+    for (int q = 0; q < G; ++q) {
+      const float sq = wave_sum(acc[q]);
+      if (lane == 0 && q < nk) xo[q] = sq;
+    }
   }
 }
 
@@ -1241,24 +1273,29 @@ struct Layout {
 int proj_tiles(int n, int J, int bj = 64) { return ((J + bj - 1) / bj) * ((n + PJ_BN - 1) / PJ_BN); }
 
 // Split the gather projections' reduction so that about 1024 workgroups run
-// even when the batch is small; never more than 16 slices.
-int proj_splits(const brisk_corrector& c, int B, int L, int K) {
+// even when the batch is small; never more than 16 slices.  Only the jobs
+// that run count: with the per-token tables the candidates' and anchors'
+// projections are not computed, and the hidden-state projection alone would
+// otherwise run unsplit on a few dozen workgroups (at 4096 rows it was the
+// longest part of the launch).
+int proj_splits(const brisk_corrector& c, int B, int L, int K, bool tab) {
   const int rows = B * L, NC = rows * K;
-  const int tiles = proj_tiles(NC, c.d_tproj) + proj_tiles(B, c.d_tproj) + proj_tiles(NC, c.rank) +
-                    proj_tiles(rows, c.d_hproj) + 2 * proj_tiles(B, c.d_state);
+  int tiles = proj_tiles(rows, c.d_hproj) + 2 * proj_tiles(B, c.d_state);
+  if (!tab) tiles += proj_tiles(NC, c.d_tproj) + proj_tiles(B, c.d_tproj) + proj_tiles(NC, c.rank);
   int sp = 1024 / (tiles > 0 ? tiles : 1);
   return sp < 1 ? 1 : (sp > 16 ? 16 : sp);
 }
 
-Layout rerank_layout(const brisk_corrector& c, int B, int L, int K) {
+Layout rerank_layout(const brisk_corrector& c, int B, int L, int K, bool tab) {
   const size_t rows = static_cast<size_t>(B) * L, NC = rows * K, NP = NC + B;
   const size_t ds = c.d_state;
   Layout l{};
-  l.splits = proj_splits(c, B, L, K);
+  l.splits = proj_splits(c, B, L, K, tab);
   const size_t S = l.splits;
   auto pad = [](size_t n) { return (n + 63) / 64 * 64; };
-  l.sPE = pad(NP * c.d_tproj);
-  l.sPC = pad(NC * c.rank);
+  // with the tables no candidate or anchor is projected
+  l.sPE = tab ? 0 : pad(NP * c.d_tproj);
+  l.sPC = tab ? 0 : pad(NC * c.rank);
   l.sPH = pad(rows * c.d_hproj);
   l.sU0 = pad(2 * static_cast<size_t>(B) * ds);
   size_t off = 0;
@@ -1289,8 +1326,10 @@ void launch_scan(const ScanArgs& sa, int B, int nw, hipStream_t s) {
 
 }  // namespace
 
+// Large enough for either path, so a workspace sized before the tables were
+// prepared (or after they were dropped) still fits.
 size_t rerank_workspace_bytes(const brisk_corrector& c, int B, int L, int K) {
-  return rerank_layout(c, B, L, K).total;
+  return std::max(rerank_layout(c, B, L, K, false).total, rerank_layout(c, B, L, K, true).total);
 }
 
 void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint16_t* ctx_hidden,
@@ -1299,7 +1338,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
                    int V, int32_t* selected, float* refined, float* gamma, float* resid,
                    const int32_t* verifier, int32_t* accept_len, int32_t* correction, void* ws,
                    hipStream_t s) {
-  const Layout lay = rerank_layout(c, B, L, K);
+  const bool tab = c.tables != nullptr;
+  const Layout lay = rerank_layout(c, B, L, K, tab);
   char* base = static_cast<char*>(ws);
   auto F = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
   const int rows = B * L, NC = rows * K, NP = NC + B;
@@ -1313,7 +1353,6 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   const size_t sPE = lay.sPE, sPC = lay.sPC, sPH = lay.sPH, sU0 = lay.sU0;
   // With the per-token tables, every per-candidate and per-anchor lift is a
   // table row: the projections of candidates and anchors are not computed.
-  const bool tab = c.tables != nullptr;
   const int n_cand = tab ? 0 : NC, n_anch = tab ? 0 : B;
   ProjJobs pj{};
   pj.d = d;
@@ -1331,10 +1370,13 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
     const int t = proj_tiles(pj.job[j].n, pj.job[j].J, bj);
     max_tiles = t > max_tiles ? t : max_tiles;
   }
-  pj.cross = CrossJob{lm_head, hidden, cand_id, anchor_tok, B, L, K, V, F(lay.X)};
-  // the cross-logit row needs (NP + 3) / 4 workgroups of four wavefronts
-  // (each loops over more when the grid is capped at about 4096 of them)
-  const int cross_x = std::min(((NP + 3) / 4 + S - 1) / S, (4096 + S - 1) / S);
+  const int group = NC >= 4096 ? 8 : 1;
+  pj.cross = CrossJob{lm_head, hidden, cand_id, anchor_tok, B, L, K, V, F(lay.X), group};
+  // the cross-logit row needs a wavefront per row and group of candidates,
+  // and one per anchor, four to a workgroup (each loops over more when the
+  // grid is capped at about 4096 workgroups)
+  const int cross_items = rows * ((K + group - 1) / group) + B;
+  const int cross_x = std::min(((cross_items + 3) / 4 + S - 1) / S, (4096 + S - 1) / S);
   const int gx = std::max(max_tiles, cross_x);
   if (bj == 128)
     hipLaunchKernelGGL(gather_proj_kernel<128>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
