@@ -481,24 +481,64 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         float pt[C::TR];
 #pragma unroll
         for (int y = 0; y < C::TR; ++y) pt[y] = s_pthr[wr * C::WR + y * 16 + l15];
+        const int vl0 = v0 + wv * C::WV + 4 * (lane >> 4);
+        if (vend - v0 < C::BV) {  // the share's last tile: rows past its end never enter
 #pragma unroll
-        for (int x = 0; x < C::TV; ++x) {
+          for (int x = 0; x < C::TV; ++x)
 #pragma unroll
-          for (int y = 0; y < C::TR; ++y) {
-            const floatx4 a4 = acc[x][y];
-            // one compare per four logits decides the common case
-            if (fmaxf(fmaxf(a4[0], a4[1]), fmaxf(a4[2], a4[3])) >= pt[y]) {
+            for (int q = 0; q < 4; ++q)
+              if (vl0 + x * 16 + q >= vend)
+#pragma unroll
+                for (int y = 0; y < C::TR; ++y) acc[x][y][q] = -3.0e38f;
+        }
+        // Per position of the lane, without branches: how many of its 16
+        // logits reach the threshold, the last of them and the largest logit.
+        // (Branching per block of logits made the whole wavefront walk every
+        // block some lane had a survivor in: about 2000 instructions a tile.)
+        int cnt[C::TR], last[C::TR];
+        float mx[C::TR];
+#pragma unroll
+        for (int y = 0; y < C::TR; ++y) {
+          int c = 0, li = 0;
+          float m = acc[0][y][0];
+#pragma unroll
+          for (int x = 0; x < C::TV; ++x)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float v = acc[x][y][q];
+              const bool ge = v >= pt[y];
+              c += ge ? 1 : 0;
+              li = ge ? x * 16 + q : li;
+              m = fmaxf(m, v);
+            }
+          cnt[y] = c;
+          last[y] = li;
+          mx[y] = m;
+        }
+        // one queue reservation per position, issued back to back (adding 0
+        // where the lane has no survivor), then the keys stored
+        int base[C::TR];
+#pragma unroll
+        for (int y = 0; y < C::TR; ++y) base[y] = atomicAdd(&s_cnt[wr * C::WR + y * 16 + l15], cnt[y]);
+#pragma unroll
+        for (int y = 0; y < C::TR; ++y) {
+          const int p = wr * C::WR + y * 16 + l15;
+          if (cnt[y] == 1) {  // the only survivor is the largest logit
+            if (base[y] < C::QCAP) sq[p * C::QCAP + base[y]] = make_key(mx[y], static_cast<uint32_t>(vl0 + last[y]));
+            else s_flag[0] = 1;
+          } else if (cnt[y] > 1) {
+            int idx = base[y];
+#pragma unroll
+            for (int x = 0; x < C::TV; ++x)
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
-                const int vid = v0 + wv * C::WV + x * 16 + 4 * (lane >> 4) + q;
-                if (a4[q] >= pt[y] && vid < vend) {
-                  const int p = wr * C::WR + y * 16 + l15;
-                  const int idx = atomicAdd(&s_cnt[p], 1);
-                  if (idx < C::QCAP) sq[p * C::QCAP + idx] = make_key(a4[q], static_cast<uint32_t>(vid));
+                if (acc[x][y][q] >= pt[y]) {
+                  if (idx < C::QCAP)
+                    sq[p * C::QCAP + idx] = make_key(acc[x][y][q], static_cast<uint32_t>(vl0 + x * 16 + q));
                   else s_flag[0] = 1;
+                  ++idx;
                 }
               }
-            }
           }
         }
         lds_sync();
@@ -526,16 +566,26 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         // a queue overflowed: the whole tile takes the full path below
       }
     }
-#pragma unroll
+    // Large-row tile: one copy of the consume loop, run once per accumulator
+    // block (its LDS store keeps static register indices); this path runs on
+    // the first tile and after an overflow, and unrolling it per block made
+    // the kernel several times larger.  Smaller tiles unroll it.
+    constexpr bool kOneConsume = C::BR >= 128;
+#pragma unroll (kOneConsume ? 1 : C::TV)
     for (int x = 0; x < C::TV; ++x) {
 #pragma unroll
-      for (int y = 0; y < C::TR; ++y) {
-        const int p = wr * C::WR + y * 16 + l15;
-        *reinterpret_cast<floatx4*>(sE + p * C::EPI_V + epi_slot(p, wv * 4 + (lane >> 4)) * 4) = acc[x][y];
-        acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+      for (int xs = 0; xs < C::TV; ++xs) {
+        if (xs == x) {
+#pragma unroll
+          for (int y = 0; y < C::TR; ++y) {
+            const int p = wr * C::WR + y * 16 + l15;
+            *reinterpret_cast<floatx4*>(sE + p * C::EPI_V + epi_slot(p, wv * 4 + (lane >> 4)) * 4) = acc[xs][y];
+            acc[xs][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+          }
+        }
       }
       lds_sync();
-#pragma unroll kColUnroll
+#pragma unroll (kOneConsume ? 1 : kColUnroll)
       for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) consume(sE, x, col, v0, vend);
       // Share the floors of a row's TPP lists: each thread's floor bounds the
       // row's KP-th largest key from below, so the largest of them filters
