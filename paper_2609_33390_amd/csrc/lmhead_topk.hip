@@ -65,7 +65,11 @@ struct TileCfg {
   // Per-position thresholds, queue counters and an overflow flag of the
   // filtered epilogue (see the kernel), after the floors.
   static constexpr int POS_OFF = THR_OFF + NT * 4;
-  static constexpr int LDS_BYTES = POS_OFF + BR * 8 + 16;
+  // Filtered epilogue: the list of the second thread of every position as
+  // floats, [BR][16], read by the first to bound the position's KP-th key.
+  static constexpr int U_OFF = POS_OFF + BR * 8 + 16;
+  static constexpr int U_BYTES = BR >= 128 ? BR * 16 * 4 : 0;
+  static constexpr int LDS_BYTES = U_OFF + U_BYTES;
   // Sampling pass: each thread keeps up to CKR candidate ids of its row in
   // registers, so testing a token against them touches no memory (a global
   // load there waits for every copy in flight, and so does an LDS read, which
@@ -133,6 +137,41 @@ constexpr bool kRowThreshold = true;  // applied where TPP <= 2 (see the epilogu
 template <class C, int KP>
 constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 + C::NT * 8 <= C::LDS_BYTES;
 
+// Bitonic sort of N floats into descending order, in registers.
+template <int N>
+__device__ __forceinline__ void sort_desc(float (&a)[N]) {
+#pragma unroll
+  for (int k = 2; k <= N; k <<= 1)
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1)
+#pragma unroll
+      for (int i = 0; i < N; ++i) {
+        const int l = i ^ j;
+        if (l > i) {
+          const float hi = fmaxf(a[i], a[l]), lo = fminf(a[i], a[l]);
+          const bool down = (i & k) == 0;
+          a[i] = down ? hi : lo;
+          a[l] = down ? lo : hi;
+        }
+      }
+}
+
+// R-th largest (R >= 1) of the union of two descending lists of N floats:
+// taking j entries from a and R - j from b, min(a[j-1], b[R-j-1]) has at
+// least R entries at or above it, and the best split reaches the R-th.
+template <int N, int R>
+__device__ __forceinline__ float union_rank(const float (&a)[N], const float (&b)[N]) {
+  static_assert(R >= 1 && R <= 2 * N, "rank within the union");
+  float t = -INFINITY;
+#pragma unroll
+  for (int j = (R > N ? R - N : 0); j <= (R < N ? R : N); ++j) {
+    const float x = j > 0 ? a[j > 0 ? j - 1 : 0] : INFINITY;
+    const float y = R - j > 0 ? b[R - j > 0 ? R - j - 1 : 0] : INFINITY;
+    t = fmaxf(t, fminf(x, y));
+  }
+  return t;
+}
+
 // Verifier rows of stochastic verification: logits are scaled by 1/T, each
 // thread also keeps a running log-sum-exp (max, scaled sum) of its logits,
 // and the keys rank s + G (a Gumbel variate per token from Philox4x32-10
@@ -197,15 +236,15 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     int n_parts, SampleArgs sa) {
   __shared__ __align__(16) unsigned char smem[C::LDS_BYTES];
   float* const s_thr = reinterpret_cast<float*>(smem + C::THR_OFF);  // list floors, [position][TPP]
-  // Filtered epilogue (large-row tiles, plain pass): from the second tile on,
-  // each lane tests its own accumulators against its positions' thresholds
-  // (the largest list floor of the position, a lower bound of its KP-th
-  // largest key) and queues only the survivors, which the position's list
-  // owners then fold.  A tile whose queues overflow takes the full path.
-  // With 16 keys per list the kernel spills 112 bytes per lane, which costs
-  // far less than the full epilogue on every tile (512 rows x 152064 tokens:
-  // 1026 -> 768 us); longer lists keep the full path.
+  // Filtered epilogue (large-row tiles, plain pass): each lane tests its own
+  // accumulators against its positions' thresholds (lower bounds of each
+  // position's KP-th largest logit: a seed on the first tile, then the KP-th
+  // of the position's two lists) and queues only the survivors, which the
+  // position's list owners then fold.  A tile whose queues overflow, and a
+  // first tile that is not whole, take the full path.  Lists of up to 16
+  // keys; longer lists keep the full path on every tile.
   constexpr bool kFilt = !SAMPLE && C::BR >= 128 && C::EPI_ALIAS && KP <= 16;
+  constexpr bool kSeed = kFilt;
   float* const s_pthr = reinterpret_cast<float*>(smem + C::POS_OFF);        // [BR]
   int* const s_cnt = reinterpret_cast<int*>(smem + C::POS_OFF + C::BR * 4);  // [BR]
   int* const s_flag = reinterpret_cast<int*>(smem + C::POS_OFF + C::BR * 8);
@@ -378,7 +417,32 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     consume(sD + x * C::BR * C::EPI_V, x, esub * 4 + (i % kColFull) * C::TPP * 4, pend_v0, pend_end);
   };
 
+  // Filtered epilogue: the position's threshold for the next tile, the
+  // KP-th largest key of its two lists together (every list entry is a
+  // logit of the position, so the KP-th of any of them bounds the KP-th of
+  // the whole vocabulary from below); also clears the position's queue.
+  auto row_bound = [&]() {
+    float* const s_u = reinterpret_cast<float*>(smem + C::U_OFF);
+    if (esub == 1) {
+#pragma unroll
+      for (int j = 0; j < KP; ++j) s_u[ep * 16 + j] = list_floor(list[j]);
+    }
+    lds_sync();
+    if (esub == 0) {
+      float a[KP], b[KP];
+#pragma unroll
+      for (int j = 0; j < KP; ++j) {
+        a[j] = list_floor(list[j]);
+        b[j] = s_u[ep * 16 + j];
+      }
+      thr = fmaxf(thr, union_rank<KP, KP>(a, b));
+      s_pthr[ep] = row_ok ? thr : INFINITY;  // padding rows (all logits 0) queue nothing
+      s_cnt[ep] = 0;
+    }
+  };
+
   if constexpr (kFilt) {
+    static_assert(!kFilt || (C::TPP == 2 && KP <= 16 && C::WAVES_V == 4), "filtered epilogue layout");
     for (int i = tid; i < C::BR; i += C::NT) {
       s_pthr[i] = -INFINITY;
       s_cnt[i] = 0;
@@ -474,10 +538,58 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       sE = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
     }
     if constexpr (kFilt) {
-      if (tl > 0) {
+      const bool whole = vend - v0 == C::BV;
+      if (tl > 0 || (kSeed && whole)) {
         // lane l holds, for position wr*WR + y*16 + l%16, the logits of
         // vocabulary rows wv*WV + x*16 + 4*(l/16) + q of the tile
         uint64_t* const sq = reinterpret_cast<uint64_t*>(sE);
+        if (kSeed && whole) {
+          // Seed from the tile itself: each of the 16 lanes that hold a
+          // position's 256 logits offers its M largest, and the KP-th
+          // largest of those 16 * M logits bounds the position's KP-th from
+          // below.  With M = 2 for 16 keys (one otherwise) about KP + 2
+          // logits of normally spread rows pass it, well inside the queues,
+          // whatever the earlier tiles left; an unlucky position only sends
+          // the tile down the full path.
+          constexpr int M = KP > 8 ? 2 : 1;
+          float* const s_seed = sE;  // [BR][16 * M], slots permuted per position
+          const int h = wv * 4 + (lane >> 4);
+#pragma unroll
+          for (int y = 0; y < C::TR; ++y) {
+            float t1 = -INFINITY, t2 = -INFINITY;
+#pragma unroll
+            for (int x = 0; x < C::TV; ++x)
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                const float v = acc[x][y][q];
+                if constexpr (M == 2) t2 = fmaxf(t2, fminf(t1, v));
+                t1 = fmaxf(t1, v);
+              }
+            const int p = wr * C::WR + y * 16 + l15;
+            const int slot = h ^ (p & 15);  // spreads a store's 16 positions over the banks
+            if constexpr (M == 2) *reinterpret_cast<float2*>(s_seed + p * 32 + slot * 2) = make_float2(t1, t2);
+            else s_seed[p * 16 + slot] = t1;
+          }
+          lds_sync();
+          if (esub == 0) {
+            float a[8 * M], b[8 * M];
+            const floatx4* src = reinterpret_cast<const floatx4*>(s_seed + ep * 16 * M);
+#pragma unroll
+            for (int c = 0; c < 4 * M; ++c) {
+              const floatx4 f = src[c];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                if (c < 2 * M) a[c * 4 + q] = f[q];
+                else b[(c - 2 * M) * 4 + q] = f[q];
+              }
+            }
+            sort_desc(a);
+            sort_desc(b);
+            thr = fmaxf(thr, union_rank<8 * M, KP>(a, b));
+            s_pthr[ep] = row_ok ? thr : INFINITY;
+          }
+          lds_sync();
+        }
         float pt[C::TR];
 #pragma unroll
         for (int y = 0; y < C::TR; ++y) pt[y] = s_pthr[wr * C::WR + y * 16 + l15];
@@ -548,23 +660,16 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
             const uint64_t key = sq[ep * C::QCAP + i];
             if (key > list[KP - 1]) list_insert(list, key);
           }
-          thr = fmaxf(thr, list_floor(list[KP - 1]));
 #pragma unroll
           for (int x = 0; x < C::TV; ++x)
 #pragma unroll
             for (int y = 0; y < C::TR; ++y) acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
-          s_thr[ep * C::TPP + esub] = thr;
-          lds_sync();  // queues read, floors written
-#pragma unroll
-          for (int e = 0; e < C::TPP; ++e) thr = fmaxf(thr, s_thr[ep * C::TPP + e]);
-          if (esub == 0) {
-            s_pthr[ep] = thr;
-            s_cnt[ep] = 0;
-          }
-          continue;  // the next tile's slices begin with a barrier
+          row_bound();  // its barrier also ends every read of the queues
+          continue;     // the next tile's slices begin with a barrier
         }
         // a queue overflowed: the whole tile takes the full path below
       }
+      thr = fmaxf(thr, s_pthr[ep]);  // the position's bound skips logits early
     }
     // Large-row tile: one copy of the consume loop, run once per accumulator
     // block (its LDS store keeps static register indices); this path runs on
@@ -600,12 +705,9 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       }
     }
     if constexpr (kFilt) {
-      // thresholds for the next tile; counters and flag cleared (read by
-      // every thread before the last barrier above)
-      if (esub == 0) {
-        s_pthr[ep] = thr;
-        s_cnt[ep] = 0;
-      }
+      // thresholds for the next tile; counters and flag cleared (the flag
+      // was read by every thread before the barriers above)
+      row_bound();
       if (tid == 0) s_flag[0] = 0;
     }
   }

@@ -274,6 +274,37 @@ def test_propose_monotone_logits(order, K):
     check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
 
 
+@pytest.mark.parametrize("K", [8, 16])
+def test_propose_tied_groups_overflow(K):
+    # 300 rows (a second row tile of 44 rows and 212 padding positions) over
+    # three vocabulary tiles per workgroup.  In the first third of the
+    # vocabulary every run of 64 tokens shares one lm_head row, so a tile's
+    # logits tie in blocks of 64: a whole block reaches any bound, more than
+    # a survivor queue holds, and those tiles take the full path; the rest of
+    # the vocabulary is spread normally and filtered.  Ties go to the lower id.
+    rows, d, V = 300, 64, (1 << 17) + 37
+    g = torch.Generator(device="cpu").manual_seed(43 + K)
+    H = torch.randn(rows, d, generator=g).to(torch.bfloat16)
+    W = torch.randn(V, d, generator=g) * 0.05
+    cut = V // 3
+    # (scaled up so that the best group often beats the spread part)
+    W[:cut] = 1.5 * W[:cut][torch.arange(cut) // 64 * 64]
+    W = W.to(torch.bfloat16)
+    cl, ci = brisk.propose_block(H.to(DEV), W.to(DEV), K)
+    torch.cuda.synchronize()
+    Hb, Wb = synth.bf16_bits(H), synth.bf16_bits(W)
+    ol = oracle.lm_logits(oracle.bf16_to_f64(Hb), Wb)
+    check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
+    # the tied head of some rows: the K lowest ids of its group, in order
+    tied = 0
+    for r in range(rows):
+        c = ci[r].cpu().numpy()
+        if c[0] < cut and ol[r, c[0]] == ol[r, c[K - 1]]:
+            assert list(c) == list(range(c[0], c[0] + K))
+            tied += 1
+    assert tied > rows // 10
+
+
 # Relative part of the score bound for corrector weights far beyond the
 # workloads' (std 0.3 at d_state 320 over 40 positions): refined scores reach
 # about 4.4e3 there, and the gate's fp32 dot product of length d_state + 5
