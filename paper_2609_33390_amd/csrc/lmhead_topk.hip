@@ -127,6 +127,22 @@ __device__ __forceinline__ int xcd_remap(int bid, int nblocks) {
   return (bid % NXCD) * per + bid / NXCD;
 }
 
+// Row tile and vocabulary group of a logical workgroup.  The workgroups of
+// one XCD run in near lockstep over the reduction, so per slice the XCD's L2
+// fetches one hidden-state slice per row tile and one lm_head slice per group
+// among them, and serves every other request: 32 workgroups as 8 row tiles x
+// 4 groups fetch 12 slices, against 18 as 16 x 2 (4096 rows: 1 -> 0.98 of
+// the pass time).  Other grids take row tiles fastest.
+__device__ __forceinline__ void tile_of(int logical, int nblocks, int n_rtiles, int n_groups, int& rt, int& group) {
+  rt = logical % n_rtiles;
+  group = logical / n_rtiles;
+  if (nblocks == 8 * 32 && n_rtiles % 8 == 0 && n_groups % 4 == 0) {
+    const int i = logical % 32, blk = logical / 32, nrb = n_rtiles / 8;
+    rt = (blk % nrb) * 8 + i % 8;
+    group = (blk / nrb) * 4 + i / 8;
+  }
+}
+
 // Equal vocabulary shares for weight-streaming shapes, and list floors shared
 // among the epilogue threads of a row (both described where they are used).
 constexpr bool kEvenShares = true;
@@ -254,8 +270,8 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wv = wave % C::WAVES_V, wr = wave / C::WAVES_V;
   const int logical = xcd_remap(blockIdx.x, gridDim.x);
-  const int rt = logical % n_rtiles;
-  const int group = logical / n_rtiles;
+  int rt, group;
+  tile_of(logical, static_cast<int>(gridDim.x), n_rtiles, n_groups, rt, group);
   const int r0 = rt * C::BR;
   // Vocabulary rows [vb, ve) of this group: runs of whole tiles, or (even)
   // equal shares cut at multiples of 16, so that every compute unit streams
