@@ -1000,11 +1000,42 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
     uint32_t key0, uint32_t key1, int32_t* __restrict__ row_accept, int32_t* __restrict__ row_resample) {
   constexpr int NT = 256, NW = NT / kWave;
   static_assert(NW == 4, "two cross-wave levels");
+  // the first NPF tokens of each wavefront have their rows in flight before
+  // anything waits (rows of up to CH * 512 elements in one batch)
+  constexpr int NPF = 3, CH = 8;
   __shared__ uint64_t sk[NW][KP];
-  __shared__ float2 s_lse[NT];
+  __shared__ float2 s_lse[NW];
   __shared__ float s_logit[kWave + 1];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int row = blockIdx.x;
+  const uint16_t* h = Hv + static_cast<size_t>(row) * d;
+  const int x = clamp_id(proposal[row], V);
+  auto token = [&](int k) { return k < K ? clamp_id(cand_id[static_cast<size_t>(row) * K + k], V) : x; };
+  auto dot8 = [](float& acc, uint4 a, uint4 b) {
+    acc += bf16_lo(a.x) * bf16_lo(b.x) + bf16_hi(a.x) * bf16_hi(b.x);
+    acc += bf16_lo(a.y) * bf16_lo(b.y) + bf16_hi(a.y) * bf16_hi(b.y);
+    acc += bf16_lo(a.z) * bf16_lo(b.z) + bf16_hi(a.z) * bf16_hi(b.z);
+    acc += bf16_lo(a.w) * bf16_lo(b.w) + bf16_hi(a.w) * bf16_hi(b.w);
+  };
+
+  // (0) loads of the verifier-logit rows: the candidates (k < K) and the
+  // proposal (k = K), token k on wavefront k % NW
+  uint4 hv[CH], wv[NPF][CH];
+#pragma unroll
+  for (int i = 0; i < CH; ++i) {
+    const int c = lane * 8 + i * kWave * 8;
+    hv[i] = c < d ? *reinterpret_cast<const uint4*>(h + c) : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int t = 0; t < NPF; ++t) {
+    const int k = wave + t * NW;
+    const uint16_t* w = W + static_cast<size_t>(k <= K ? token(k) : x) * d;
+#pragma unroll
+    for (int i = 0; i < CH; ++i) {
+      const int c = lane * 8 + i * kWave * 8;
+      wv[t][i] = k <= K && c < d ? *reinterpret_cast<const uint4*>(w + c) : make_uint4(0, 0, 0, 0);
+    }
+  }
 
   // (1) keys of s + G: per-lane lists, wave butterflies, then across waves
   const int n_keys = n_parts * KP;
@@ -1013,70 +1044,65 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
   fold_parts(list, src, n_parts, tid, NT);
+  // (2) log-sum-exp partials, combined in a fixed order: strided per thread,
+  // then a butterfly within the wavefront, then the wavefronts in order
+  float m = -INFINITY, sm = 0.f;
+  for (int i = tid; i < n_parts; i += NT) lse_combine(m, sm, lse_part[static_cast<size_t>(row) * n_parts + i]);
   wave_merge(list);
   if (lane == 0) {
 #pragma unroll
     for (int j = 0; j < KP; ++j) sk[wave][j] = list[j];
   }
-  // (2) log-sum-exp partials, combined in a fixed order
-  float m = -INFINITY, sm = 0.f;
-  for (int i = tid; i < n_parts; i += NT) lse_combine(m, sm, lse_part[static_cast<size_t>(row) * n_parts + i]);
-  s_lse[tid] = make_float2(m, sm);
-  // (3) verifier logits of the candidates (k < K) and of the proposal (k = K)
-  const uint16_t* h = Hv + static_cast<size_t>(row) * d;
-  const int x = clamp_id(proposal[row], V);
-  for (int k = wave; k <= K; k += NW) {
-    const int v = k < K ? clamp_id(cand_id[static_cast<size_t>(row) * K + k], V) : x;
-    const uint16_t* w = W + static_cast<size_t>(v) * d;
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1)
+    lse_combine(m, sm, make_float2(__shfl_xor(m, off, kWave), __shfl_xor(sm, off, kWave)));
+  if (lane == 0) s_lse[wave] = make_float2(m, sm);
+
+  // (3) the dot products: the prefetched tokens, then any further ones
+#pragma unroll
+  for (int t = 0; t < NPF; ++t) {
+    const int k = wave + t * NW;
+    if (k > K) break;
     float acc = 0.f;
-    for (int c = lane * 8; c < d; c += kWave * 8) {
-      const uint4 a = *reinterpret_cast<const uint4*>(w + c);
-      const uint4 b = *reinterpret_cast<const uint4*>(h + c);
-      acc += bf16_lo(a.x) * bf16_lo(b.x) + bf16_hi(a.x) * bf16_hi(b.x);
-      acc += bf16_lo(a.y) * bf16_lo(b.y) + bf16_hi(a.y) * bf16_hi(b.y);
-      acc += bf16_lo(a.z) * bf16_lo(b.z) + bf16_hi(a.z) * bf16_hi(b.z);
-      acc += bf16_lo(a.w) * bf16_lo(b.w) + bf16_hi(a.w) * bf16_hi(b.w);
-    }
+#pragma unroll
+    for (int i = 0; i < CH; ++i) dot8(acc, wv[t][i], hv[i]);
+    const uint16_t* w = W + static_cast<size_t>(token(k)) * d;
+    for (int c = lane * 8 + CH * kWave * 8; c < d; c += kWave * 8)
+      dot8(acc, *reinterpret_cast<const uint4*>(w + c), *reinterpret_cast<const uint4*>(h + c));
+    acc = wave_sum(acc);
+    if (lane == 0) s_logit[k] = acc;
+  }
+  for (int k = wave + NPF * NW; k <= K; k += NW) {
+    const uint16_t* w = W + static_cast<size_t>(token(k)) * d;
+    float acc = 0.f;
+    for (int c = lane * 8; c < d; c += kWave * 8)
+      dot8(acc, *reinterpret_cast<const uint4*>(w + c), *reinterpret_cast<const uint4*>(h + c));
     acc = wave_sum(acc);
     if (lane == 0) s_logit[k] = acc;
   }
   __syncthreads();
-  for (int st = NT / 2; st >= 1; st >>= 1) {
-    if (tid < st) {
-      float2 me = s_lse[tid];
-      lse_combine(me.x, me.y, s_lse[tid + st]);
-      s_lse[tid] = me;
-    }
-    __syncthreads();
-  }
   if (wave != 0) return;
+  float2 tot = s_lse[0];
+#pragma unroll
+  for (int w = 1; w < NW; ++w) lse_combine(tot.x, tot.y, s_lse[w]);
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = lane < NW ? sk[lane][j] : 0ull;
   butterfly_merge<1>(list);
   butterfly_merge<2>(list);
-  if (lane != 0) return;
 
-  // (4) decisions, in lane 0, with the accurate exp / log: where p_r and
-  // pi_r nearly cancel, the residual weight needs every bit fp32 has
-  const float lse = s_lse[0].x + logf(s_lse[0].y);
+  // (4) decisions with the accurate exp / log: where p_r and pi_r nearly
+  // cancel, the residual weight needs every bit fp32 has
+  const float lse = tot.x + logf(tot.y);
   const int32_t* ids = cand_id + static_cast<size_t>(row) * K;
   // no cand_prob: the proposal is the greedy choice, pi_r = point mass at x_r
   const float* pis = cand_prob ? cand_prob + static_cast<size_t>(row) * K : nullptr;
   auto pi_of = [&](int k, int v) { return pis ? pis[k] : (v == x ? 1.f : 0.f); };
-  float pi_x = 0.f;
-  for (int k = 0; k < K; ++k) {
-    const int v = clamp_id(ids[k], V);
-    if (v == x) pi_x += pi_of(k, v);
-  }
-  // p <= 1 holds exactly; the clamp keeps rounding (the dot products and the
-  // log-sum-exp add in different orders) from giving weight to pi = 1
-  const float p_x = fminf(1.f, expf(s_logit[K] * inv_T - lse));
-  const bool accept = pi_x <= 0.f || u_accept[row] < fminf(1.f, p_x / pi_x);
-  // residual draw: candidates from their exact weights, everyone else from
-  // the best key (no candidate enters the lists; score s + G - lse)
+  // residual draw: candidate k scored by lane k from its exact weight,
+  // everyone else from the best key (no candidate enters the lists; score
+  // s + G - lse); the best score wins, the lower id on ties
   float best = -INFINITY;
   int best_id = 0x7FFFFFFF;
-  for (int k = 0; k < K; ++k) {
+  for (int k = lane; k < K; k += kWave) {
     const int v = clamp_id(ids[k], V);
     const float w = fminf(1.f, expf(s_logit[k] * inv_T - lse)) - pi_of(k, v);
     if (w <= 0.f) continue;
@@ -1089,6 +1115,25 @@ __global__ __launch_bounds__(256) void spec_row_kernel(
       best_id = v;
     }
   }
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const float ob = __shfl_xor(best, off, kWave);
+    const int oi = __shfl_xor(best_id, off, kWave);
+    if (ob > best || (ob == best && oi < best_id)) {
+      best = ob;
+      best_id = oi;
+    }
+  }
+  if (lane != 0) return;
+  float pi_x = 0.f;
+  for (int k = 0; k < K; ++k) {
+    const int v = clamp_id(ids[k], V);
+    if (v == x) pi_x += pi_of(k, v);
+  }
+  // p <= 1 holds exactly; the clamp keeps rounding (the dot products and the
+  // log-sum-exp add in different orders) from giving weight to pi = 1
+  const float p_x = fminf(1.f, expf(s_logit[K] * inv_T - lse));
+  const bool accept = pi_x <= 0.f || u_accept[row] < fminf(1.f, p_x / pi_x);
   if (list[0] != 0) {
     const int v = key_id(list[0]);
     const float sc = key_logit(list[0]) - lse;
