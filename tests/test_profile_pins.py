@@ -6,13 +6,15 @@ from fractions import Fraction
 import numpy as np
 import pytest
 
+import fixtures
 import oracle
 
 
-@pytest.mark.parametrize("r,printed", [(0.0, 8.0), (0.10, 4.09), (0.15, 3.29), (0.20, 2.77)])
-def test_stride_equation_printed_values(r, printed):
-    # Section 2.2 prints TPF at stride N = 8 for these rejection rates
-    assert abs(oracle.tpf_stride(8, r) - printed) <= 0.005
+@pytest.mark.parametrize("N,r,printed", [tuple(float(x) for x in row) for row in fixtures.rows("tpf_stride8.txt")])
+def test_stride_equation_printed_values(N, r, printed):
+    # Section 2.2 prints TPF at stride N = 8 for these rejection rates, to two
+    # decimals (tests/golden/tpf_stride8.txt)
+    assert abs(oracle.tpf_stride(int(N), r) - printed) <= 0.005
 
 
 @pytest.mark.parametrize("N", [2, 3, 8, 17])
