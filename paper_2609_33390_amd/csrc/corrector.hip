@@ -1449,10 +1449,12 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   // random 1 KiB reads from the tables outlast that lead: at 32 rows the scan
   // took 40 instead of 23 us, with 16 keys (two rows of lead) 72 instead of
   // 36 us.  Copying the rows into the step blocks first is a parallel,
-  // bandwidth-bound pass (5 us at 32 rows, 32 us at 4096); it loses only when
-  // there are many short sequences (4096 rows as 256 x 16: 165 against
-  // 140 us for the whole rerank), where the gathering scan is used.
-  const bool scan_gathers = tab && pc && K <= 8 && B >= 128;
+  // bandwidth-bound pass whose cost grows with the batch (5 us at 32 rows,
+  // 17 us at 2048, 32 us at 4096), against a latency the gathering scan pays
+  // once per step whatever the batch: the whole rerank took 89.5 against
+  // 76.3 us with gathering at 64 x 32 rows, and 165 against 140 us at
+  // 256 x 16, so the scan gathers from 64 sequences on.
+  const bool scan_gathers = tab && pc && K <= 8 && B >= 64;
   if (tab && !scan_gathers) {
     // the scan reads whole step blocks: copy the table rows in
     const FillArgs fa{c.tables, cand_id, anchor_tok, SB, F(lay.TZA), F(lay.THA), rows, K, B, V, ds,
