@@ -1,7 +1,8 @@
 """GPU checks of the launch structure: the LM-head pass and the merge called
 separately equal brisk_propose_block, and a hipGraph capture of the whole step
-(propose, rerank, verify; the last two also as the single rerank_verify call)
-reproduces the eager results on every replay."""
+(propose, rerank, verify; the last two also as the single rerank_verify call,
+with and without the corrector's per-token tables) reproduces the eager
+results on every replay."""
 import pytest
 import torch
 
@@ -27,12 +28,18 @@ def test_split_launches_equal_the_composed_call(name):
     assert torch.equal(cl, cl2) and torch.equal(ci, ci2)
 
 
-@pytest.mark.parametrize("fused", [False, True])
-@pytest.mark.parametrize("name", ["tiny-d64-v512", "llada8b-b1-l32"])
-def test_graph_replay_matches_eager(name, fused):
+@pytest.mark.parametrize("name,fused,tables", [
+    ("tiny-d64-v512", False, False), ("tiny-d64-v512", True, False),
+    ("llada8b-b1-l32", False, False), ("llada8b-b1-l32", True, False),
+    # with the corrector's per-token tables: the step blocks filled from them,
+    # and (64 sequences) the scan gathering the table rows itself
+    ("tiny-d64-v512", True, True), ("llada8b-b1-l32", True, True), ("llada8b-b64-l32", True, True)])
+def test_graph_replay_matches_eager(name, fused, tables):
     wl = synth.WORKLOADS[name]
     blk = synth.make_block(wl, "cuda")
     corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
+    if tables:
+        corr.prepare(blk.W, blk.E)
     rows, K = wl.rows, wl.K
     dev = torch.device("cuda")
     cl = torch.empty(rows, K, dtype=torch.float32, device=dev)
