@@ -238,6 +238,9 @@ RAGGED = [
     (17, 328, 5000, 8), (32, 584, 70001, 8), (3, 256, 129, 4), (1, 4104, 3001, 8),
     # the large-row tile with 16 keys per list: the filtered epilogue
     (200, 136, 40000, 16), (513, 72, 9000, 16),
+    # the large-row tile with 4-key lists (its seed is the 4th largest of 16
+    # lane maxima), one with a second row tile holding a single row
+    (100, 72, 20000, 3), (257, 64, 50000, 4),
 ]
 
 
