@@ -555,11 +555,13 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     }
     if constexpr (kFilt) {
       const bool whole = vend - v0 == C::BV;
-      if (tl > 0 || (kSeed && whole)) {
+      // seed the first two tiles; after them the two lists bound tightly
+      const bool seed = kSeed && whole && tl < 2;
+      if (tl > 0 || seed) {
         // lane l holds, for position wr*WR + y*16 + l%16, the logits of
         // vocabulary rows wv*WV + x*16 + 4*(l/16) + q of the tile
         uint64_t* const sq = reinterpret_cast<uint64_t*>(sE);
-        if (kSeed && whole) {
+        if (seed) {
           // Seed from the tile itself: each of the 16 lanes that hold a
           // position's 256 logits offers its M largest, and the KP-th
           // largest of those 16 * M logits bounds the position's KP-th from
