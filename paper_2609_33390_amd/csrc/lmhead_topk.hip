@@ -254,8 +254,9 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   float* const s_thr = reinterpret_cast<float*>(smem + C::THR_OFF);  // list floors, [position][TPP]
   // Filtered epilogue (large-row tiles, plain pass): each lane tests its own
   // accumulators against its positions' thresholds (lower bounds of each
-  // position's KP-th largest logit: a seed on the first tile, then the KP-th
-  // of the position's two lists) and queues only the survivors, which the
+  // position's KP-th largest logit: the KP-th of the position's two lists,
+  // raised on the first two tiles by a seed from the tile itself) and
+  // queues only the survivors, which the
   // position's list owners then fold.  A tile whose queues overflow, and a
   // first tile that is not whole, take the full path.  Lists of up to 16
   // keys; longer lists keep the full path on every tile.
@@ -690,9 +691,10 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       thr = fmaxf(thr, s_pthr[ep]);  // the position's bound skips logits early
     }
     // Large-row tile: one copy of the consume loop, run once per accumulator
-    // block (its LDS store keeps static register indices); this path runs on
-    // the first tile and after an overflow, and unrolling it per block made
-    // the kernel several times larger.  Smaller tiles unroll it.
+    // block (its LDS store keeps static register indices); on this tile the
+    // path runs after an overflow, on a first tile that is not whole and for
+    // lists longer than 16 keys, and unrolling it per block made the kernel
+    // several times larger.  Smaller tiles unroll it.
     constexpr bool kOneConsume = C::BR >= 128;
 #pragma unroll (kOneConsume ? 1 : C::TV)
     for (int x = 0; x < C::TV; ++x) {
