@@ -453,12 +453,14 @@ def main():
     subs = {}
     for name in [n for n in args.configs.split(",") if n and n != args.workload]:
         blk = synth.make_block(synth.WORKLOADS[name], dev)
-        _, r = measure(brisk, blk, args.steps, args.warmup, graph, not args.no_tables)
+        st_sub, r = measure(brisk, blk, args.steps, args.warmup, graph, not args.no_tables)
         r["lmhead"]["traffic"] = counter_traffic(blk.wl)
+        if not args.no_extras:
+            r["spec_verify"] = time_spec_verify(brisk, st_sub)
         subs[name] = r
         print(f"# {name}: {r['ms_per_step']:.4f} ms/step, step roofline {r['step_roofline']['frac']}, "
               f"LM-head {r['lmhead']['frac']} of {r['lmhead']['bound']}", file=sys.stderr, flush=True)
-        del blk, _
+        del blk, st_sub
         torch.cuda.empty_cache()
 
     wl = synth.WORKLOADS[args.workload]

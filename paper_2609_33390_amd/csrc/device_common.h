@@ -146,12 +146,15 @@ __device__ __forceinline__ float sigmoidf_(float x) { return 1.0f / (1.0f + __ex
 // 32x32 -> 64-bit products (multipliers 0xD2511F53, 0xCD9E8D57) and a Weyl
 // key schedule (increments 0x9E3779B9, 0xBB67AE85).
 // ---------------------------------------------------------------------------
+// Each product is one 64-bit multiply-add (half the quarter-rate
+// instructions of separate high and low halves).
 __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1) {
 #pragma unroll
   for (int i = 0; i < 10; ++i) {
-    const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
-    const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
-    c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    const uint64_t p0 = static_cast<uint64_t>(0xD2511F53u) * c.x;
+    const uint64_t p1 = static_cast<uint64_t>(0xCD9E8D57u) * c.z;
+    c = make_uint4(static_cast<uint32_t>(p1 >> 32) ^ c.y ^ k0, static_cast<uint32_t>(p1),
+                   static_cast<uint32_t>(p0 >> 32) ^ c.w ^ k1, static_cast<uint32_t>(p0));
     k0 += 0x9E3779B9u;
     k1 += 0xBB67AE85u;
   }
@@ -159,10 +162,13 @@ __device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1
 }
 
 // Gumbel variate of a generator word: U = (w / 512 + 1/2) / 2^23 lies
-// strictly inside (0, 1) and is exact in single precision; G = -log(-log U).
+// strictly inside (0, 1) and is exact in single precision; G = -log(-log U),
+// both logarithms from the hardware base-2 logarithm.  U >= 2^-24 and
+// -log U >= 2^-24 are normal numbers, so it needs no subnormal scaling.
 __device__ __forceinline__ float gumbel_of(uint32_t w) {
+  constexpr float kLn2 = 0.69314718055994531f;
   const float U = (static_cast<float>(w >> 9) + 0.5f) * (1.0f / 8388608.0f);
-  return -__logf(-__logf(U));
+  return -kLn2 * __builtin_amdgcn_logf(-kLn2 * __builtin_amdgcn_logf(U));
 }
 
 // Merge a log-sum-exp partial (max m, sum of exp(x - m)) into (m, s).

@@ -35,28 +35,37 @@ namespace brisk {
 
 namespace {
 
-template <int BV_, int BR_, int WAVES_V_, int WAVES_R_, int BK_, int STAGES_>
+template <int BV_, int BR_, int WAVES_V_, int WAVES_R_, int BK_, int STAGES_, bool SPLIT_ = true>
 struct TileCfg {
   static constexpr int BV = BV_, BR = BR_, WAVES_V = WAVES_V_, WAVES_R = WAVES_R_, BK = BK_;
   static constexpr int STAGES = STAGES_;
   // the epilogue stages one 16-column accumulator block of every wave at a time
   static constexpr int EPI_V = 16 * WAVES_V;
   static constexpr int NW = WAVES_V * WAVES_R, NT = 64 * NW;
+  // Small row tiles defer a tile's top-K into the next tile's reduction
+  // loop: the whole tile of logits waits in its own buffer, [TV][BR][EPI_V]
+  // fp32, while the copies of the next tile stream.
+  static constexpr bool DEFER = BR <= 32;
+  // There the top-K runs on wavefronts of its own (SPLIT_): NCW consumer
+  // waves own the key lists and fold the staged tile while the NW compute
+  // waves issue the next tile's copies and products, one of each per SIMD.
+  // Folded by the compute waves, the fold sat on the copy loop's path: the
+  // sampling pass spent 40 of its 221 us at 32 rows on it.  NTA threads in
+  // all; NC own lists.
+  static constexpr int NCW = DEFER && SPLIT_ ? NW : 0;
+  static constexpr int NTA = 64 * (NW + NCW);
+  static constexpr int NC = NCW ? 64 * NCW : NT;
   static constexpr int WV = BV / WAVES_V, WR = BR / WAVES_R, TV = WV / 16, TR = WR / 16;
   static constexpr int CPR = BK / 8;            // 16-byte chunks per staged row
   static constexpr int RPI = 64 / CPR;          // staged rows one DMA instruction fills
   static constexpr int ROWS = BV + BR;          // staged rows per stage: lm_head tile, then hidden tile
   static constexpr int NDMA = ROWS / RPI / NW;  // DMA instructions per wave per stage
   static constexpr int STAGE_BYTES = ROWS * BK * 2;
-  static constexpr int TPP = NT / BR;           // epilogue threads per position
+  static constexpr int TPP = NC / BR;           // epilogue threads per position
   static constexpr int EPI_BYTES = BR * EPI_V * 4;  // staged logits, [BR][EPI_V] fp32
   // The epilogue reuses the stage buffer of the slice just consumed when it
   // fits (no copy targets that buffer until the next slice begins).
   static constexpr bool EPI_ALIAS = EPI_BYTES <= STAGE_BYTES;
-  // Small row tiles defer a tile's top-K into the next tile's reduction
-  // loop: the whole tile of logits waits in its own buffer, [TV][BR][EPI_V]
-  // fp32, while the copies of the next tile stream.
-  static constexpr bool DEFER = BR <= 32;
   static constexpr int DEF_BYTES = DEFER ? BR * BV * 4 : 0;
   // the epilogue's list floors, [BR][TPP] fp32, follow the buffers (one
   // LDS object for the whole kernel: a second one makes the compiler wait
@@ -64,7 +73,7 @@ struct TileCfg {
   static constexpr int THR_OFF = STAGES * STAGE_BYTES + (DEFER ? DEF_BYTES : (EPI_ALIAS ? 0 : EPI_BYTES));
   // Per-position thresholds, queue counters and an overflow flag of the
   // filtered epilogue (see the kernel), after the floors.
-  static constexpr int POS_OFF = THR_OFF + NT * 4;
+  static constexpr int POS_OFF = THR_OFF + NC * 4;
   // Filtered epilogue: the list of the second thread of every position as
   // floats, [BR][16], read by the first to bound the position's KP-th key.
   static constexpr int U_OFF = POS_OFF + BR * 8 + 16;
@@ -83,6 +92,7 @@ struct TileCfg {
   static_assert(NT % BR == 0 && (TPP & (TPP - 1)) == 0, "epilogue thread mapping");
   static_assert(BK % 32 == 0 && (CPR == 4 || CPR == 8 || CPR == 16 || CPR == 32), "reduction slice");
   static_assert(EPI_V % (4 * TPP) == 0 && EPI_V >= 32, "epilogue chunking");
+  static_assert(!DEFER || TPP % 4 == 0, "row floors of the deferred fold are read as float4");
   static_assert((STAGES - 2) * NDMA <= 63, "vmcnt range");
   static_assert(LDS_BYTES <= 160 * 1024, "LDS budget");
 };
@@ -146,12 +156,12 @@ __device__ __forceinline__ void tile_of(int logical, int nblocks, int n_rtiles, 
 // Equal vocabulary shares for weight-streaming shapes, and list floors shared
 // among the epilogue threads of a row (both described where they are used).
 constexpr bool kEvenShares = true;
-constexpr bool kRowThreshold = true;  // applied where TPP <= 2 (see the epilogue)
+constexpr bool kRowThreshold = true;  // where TPP <= 2, and in the deferred fold
 
 // Whether the per-position lists fit in LDS for the in-workgroup merge (the
 // stage buffers are idle by then).
 template <class C, int KP>
-constexpr bool kWgMerge = C::TPP > 1 && C::NT * KP * 8 + C::NT * 8 <= C::LDS_BYTES;
+constexpr bool kWgMerge = C::TPP > 1 && C::NC * KP * 8 + C::NC * 8 <= C::LDS_BYTES;
 
 // Bitonic sort of N floats into descending order, in registers.
 template <int N>
@@ -246,7 +256,7 @@ __device__ __forceinline__ bool is_candidate_reg(const int (&ids)[N], uint64_t m
 // One workgroup per compute unit (the LDS footprint allows no more), so the
 // compiler may split the whole register file among the workgroup's waves.
 template <class C, int KP, bool SAMPLE = false>
-__global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4, C::NW / 4))) void lmhead_topk_kernel(
+__global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA / 256, C::NTA / 256))) void lmhead_topk_kernel(
     const uint16_t* __restrict__ H, const uint16_t* __restrict__ W, int rows, int d, int V,
     int n_rtiles, int n_groups, int tiles_per_group, int even, uint64_t* __restrict__ partial,
     int n_parts, SampleArgs sa) {
@@ -347,7 +357,11 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   for (int kk = 0; kk < C::BK / 32; ++kk)
     lane_off[kk] = (l15 * C::CPR + swz<C::CPR>(l15, kk * 4 + (lane >> 4))) * 16;
 
-  const int ep = tid % C::BR, esub = tid / C::BR;
+  // roles (see TileCfg::NCW); without consumer waves every wave does both
+  const bool computer = C::NCW == 0 || wave < C::NW;
+  const bool consumer = C::NCW == 0 || wave >= C::NW;
+  const int ctid = C::NCW ? (consumer ? tid - C::NT : 0) : tid;  // index among the list owners
+  const int ep = ctid % C::BR, esub = ctid / C::BR;
   uint64_t list[KP];
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
@@ -368,7 +382,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   for (int k = 0; k < kCandRegs; ++k) cid_reg[k] = -1;
   const bool cand_reg = SAMPLE && sa.K <= C::CKR;
   if constexpr (SAMPLE) {
-    if (row_ok) {
+    if (consumer && row_ok) {
       cmask = candidate_mask(sa, r0 + ep, V);
       if (cand_reg) {
 #pragma unroll
@@ -430,8 +444,23 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   float* const sD = reinterpret_cast<float*>(smem + C::STAGES * C::STAGE_BYTES);
   int pend = kItems, pend_v0 = 0, pend_end = 0;
   auto consume_item = [&](int i) {
+    if (!consumer) return;
+    if constexpr (kRowThreshold) {
+      // Every list's floor bounds its row's KP-th key from below, so the
+      // largest floor the row's lists have published filters this one too
+      // (a floor being replaced is still a bound: no barrier needed).  Once
+      // the lists are full, far fewer logits reach the shared floor than a
+      // list's own, and the fold skips their keys and candidate tests.
+      const floatx4* f = reinterpret_cast<const floatx4*>(s_thr + ep * C::TPP);
+#pragma unroll
+      for (int e = 0; e < C::TPP / 4; ++e) {
+        const floatx4 t = f[e];
+        thr = fmaxf(thr, fmaxf(fmaxf(t[0], t[1]), fmaxf(t[2], t[3])));
+      }
+    }
     const int x = i / kColFull;
     consume(sD + x * C::BR * C::EPI_V, x, esub * 4 + (i % kColFull) * C::TPP * 4, pend_v0, pend_end);
+    if constexpr (kRowThreshold) s_thr[ep * C::TPP + esub] = thr;
   };
 
   // Filtered epilogue: the position's threshold for the next tile, the
@@ -458,9 +487,12 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     }
   };
 
+  if constexpr (C::DEFER && kRowThreshold) {
+    for (int i = tid; i < C::NC; i += C::NTA) s_thr[i] = -INFINITY;
+  }
   if constexpr (kFilt) {
     static_assert(!kFilt || (C::TPP == 2 && KP <= 16 && C::WAVES_V == 4), "filtered epilogue layout");
-    for (int i = tid; i < C::BR; i += C::NT) {
+    for (int i = tid; i < C::BR; i += C::NTA) {
       s_pthr[i] = -INFINITY;
       s_cnt[i] = 0;
     }
@@ -473,8 +505,10 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
 #pragma unroll
     for (int b = 0; b < C::TR; ++b) acc[a][b] = floatx4{0.f, 0.f, 0.f, 0.f};
 
+  if (computer) {
 #pragma unroll
-  for (int st = 0; st < C::STAGES - 1; ++st) issue(st);
+    for (int st = 0; st < C::STAGES - 1; ++st) issue(st);
+  }
 
   for (int tl = 0; tl < n_tiles; ++tl) {
     for (int kt = 0; kt < nk; ++kt) {
@@ -483,18 +517,19 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       // fewer younger copies exist, so wait for all)
       if (g + C::STAGES - 2 < n_tiles * nk) stage_sync<(C::STAGES - 2) * C::NDMA>();
       else stage_sync<0>();
-      issue(g + C::STAGES - 1);                  // refills the buffer slice g-1 used
+      if (computer) issue(g + C::STAGES - 1);    // refills the buffer slice g-1 used
       const unsigned char* sb = smem + (g % C::STAGES) * C::STAGE_BYTES;
       if (tail && kt == nk - 1) {
         // chunks past d hold re-read data: zero them in the lm_head tile
         unsigned char* wb = smem + (g % C::STAGES) * C::STAGE_BYTES;
         const int nz = C::CPR - tail;
-        for (int idx = tid; idx < C::BV * nz; idx += C::NT) {
+        for (int idx = tid; idx < C::BV * nz; idx += C::NTA) {
           const int R = idx / nz, c = tail + idx % nz;
           *reinterpret_cast<uint4*>(wb + (R * C::CPR + swz<C::CPR>(R, c)) * 16) = make_uint4(0, 0, 0, 0);
         }
         lds_sync();
       }
+      if (computer) {
 #pragma unroll
       for (int kk = 0; kk < C::BK / 32; ++kk) {
         // all operand fragments of this 32-wide slice first, then the MFMAs,
@@ -515,6 +550,7 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
         __builtin_amdgcn_sched_group_barrier(0x100, C::TV + C::TR, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, C::TV * C::TR, 0);
       }
+      }
       if constexpr (C::DEFER) {
         // the previous tile's top-K, spread evenly over this tile's slices
         while (pend < kItems && kt * kItems >= pend * nk) consume_item(pend++);
@@ -528,14 +564,16 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
     if constexpr (C::DEFER) {
       while (pend < kItems) consume_item(pend++);  // tiles shorter than kItems slices
       lds_sync();  // every thread has finished with the previous tile's logits
+      if (computer) {
 #pragma unroll
-      for (int x = 0; x < C::TV; ++x) {
+        for (int x = 0; x < C::TV; ++x) {
 #pragma unroll
-        for (int y = 0; y < C::TR; ++y) {
-          const int p = wr * C::WR + y * 16 + l15;
-          *reinterpret_cast<floatx4*>(sD + (x * C::BR + p) * C::EPI_V + epi_slot(p, wv * 4 + (lane >> 4)) * 4) =
-              acc[x][y];
-          acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+          for (int y = 0; y < C::TR; ++y) {
+            const int p = wr * C::WR + y * 16 + l15;
+            *reinterpret_cast<floatx4*>(sD + (x * C::BR + p) * C::EPI_V + epi_slot(p, wv * 4 + (lane >> 4)) * 4) =
+                acc[x][y];
+            acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
+          }
         }
       }
       lds_sync();
@@ -711,7 +749,8 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
       }
       lds_sync();
 #pragma unroll (kOneConsume ? 1 : kColUnroll)
-      for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4) consume(sE, x, col, v0, vend);
+      for (int col = esub * 4; col < C::EPI_V; col += C::TPP * 4)
+        consume(sE, x, col, v0, vend);
       // Share the floors of a row's TPP lists: each thread's floor bounds the
       // row's KP-th largest key from below, so the largest of them filters
       // every list of the row.  It pays on the large-row tile (two lists per
@@ -738,37 +777,39 @@ __global__ __launch_bounds__(C::NT) __attribute__((amdgpu_waves_per_eu(C::NW / 4
   const int r = r0 + ep;
   if constexpr (kWgMerge<C, KP>) {
     uint64_t* sk = reinterpret_cast<uint64_t*>(smem);
-    float2* sl = reinterpret_cast<float2*>(smem + C::NT * KP * 8);
+    float2* sl = reinterpret_cast<float2*>(smem + C::NC * KP * 8);
+    if (consumer) {
 #pragma unroll
-    for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
-    if constexpr (SAMPLE) sl[tid] = make_float2(lse_m, lse_s);
+      for (int j = 0; j < KP; ++j) sk[j * C::NC + ctid] = list[j];
+      if constexpr (SAMPLE) sl[ctid] = make_float2(lse_m, lse_s);
+    }
     lds_sync();
 #pragma unroll
     for (int s = C::TPP / 2; s >= 1; s >>= 1) {
-      if (esub < s) {
+      if (consumer && esub < s) {
         const int other = (esub + s) * C::BR + ep;
 #pragma unroll
         for (int j = 0; j < KP; ++j) {
-          const uint64_t key = sk[j * C::NT + other];
+          const uint64_t key = sk[j * C::NC + other];
           if (key > list[KP - 1]) list_insert(list, key);
         }
 #pragma unroll
-        for (int j = 0; j < KP; ++j) sk[j * C::NT + tid] = list[j];
+        for (int j = 0; j < KP; ++j) sk[j * C::NC + ctid] = list[j];
         if constexpr (SAMPLE) {
           lse_combine(lse_m, lse_s, sl[other]);
-          sl[tid] = make_float2(lse_m, lse_s);
+          sl[ctid] = make_float2(lse_m, lse_s);
         }
       }
       lds_sync();
     }
-    if (esub == 0 && r < rows) {
+    if (consumer && esub == 0 && r < rows) {
       uint64_t* dst = partial + (static_cast<size_t>(r) * n_parts + group) * KP;
 #pragma unroll
       for (int j = 0; j < KP; ++j) dst[j] = list[j];
       if constexpr (SAMPLE) sa.lse_part[static_cast<size_t>(r) * n_parts + group] = make_float2(lse_m, lse_s);
     }
   } else {
-    if (r < rows) {
+    if (consumer && r < rows) {
       const size_t part = static_cast<size_t>(r) * n_parts + static_cast<size_t>(group) * C::TPP + esub;
       uint64_t* dst = partial + part * KP;
 #pragma unroll
@@ -929,6 +970,9 @@ __global__ __launch_bounds__(64 * NW) void topk_merge_kernel(const uint64_t* __r
 // tiles of 64-wide slices (128-byte runs) and leaves more tiles for the
 // deferred top-K to hide behind.
 using SmallRows = TileCfg<64, 32, 4, 1, 256, 3>;
+// 64-key lists take 128 registers: at two waves per SIMD they would spill,
+// so that case keeps the fold in the compute waves.
+using SmallRowsUnsplit = TileCfg<64, 32, 4, 1, 256, 3, false>;
 using MidRows = TileCfg<256, 64, 4, 1, 64, 3>;      // <= 64 rows
 using LargeRows = TileCfg<256, 256, 4, 2, 64, 2>;   // many rows: MFMA bound
 
@@ -981,7 +1025,7 @@ template <class C, int KP, bool SAMPLE = false>
 void launch_tile(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, int d, int V,
                  uint64_t* partial, hipStream_t s, SampleArgs sa = SampleArgs{}) {
   const int nblocks = p.n_rtiles * p.n_groups;
-  hipLaunchKernelGGL((lmhead_topk_kernel<C, KP, SAMPLE>), dim3(nblocks), dim3(C::NT), 0, s, H, W, rows,
+  hipLaunchKernelGGL((lmhead_topk_kernel<C, KP, SAMPLE>), dim3(nblocks), dim3(C::NTA), 0, s, H, W, rows,
                      d, V, p.n_rtiles, p.n_groups, p.tiles_per_group, p.even, partial, p.n_parts, sa);
 }
 
@@ -1178,7 +1222,10 @@ template <int KP>
 void launch_kp_pass(const Plan& p, const uint16_t* H, const uint16_t* W, int rows, int d, int V,
                     uint64_t* partial, hipStream_t s) {
   switch (p.cfg) {
-    case 0: launch_tile<SmallRows, KP>(p, H, W, rows, d, V, partial, s); break;
+    case 0:
+      if constexpr (KP >= 64) launch_tile<SmallRowsUnsplit, KP>(p, H, W, rows, d, V, partial, s);
+      else launch_tile<SmallRows, KP>(p, H, W, rows, d, V, partial, s);
+      break;
     case 1: launch_tile<MidRows, KP>(p, H, W, rows, d, V, partial, s); break;
     default: launch_tile<LargeRows, KP>(p, H, W, rows, d, V, partial, s); break;
   }
