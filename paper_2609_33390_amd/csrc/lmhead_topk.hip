@@ -98,14 +98,21 @@ struct TileCfg {
 };
 
 // 16-byte slot that holds chunk c of staged row r (an involution in c).  A
-// 128-bit LDS read is served 8 lanes at a time; the MFMA operand reads put 8
-// consecutive rows at one chunk in such a group, so the eight rows of every
-// aligned run of 8 must land on eight different 16-byte bank groups (rows are
-// CPR * 16 bytes long: a bank line of 128 bytes holds 8 / CPR rows when CPR
-// < 8, and rows of 8 chunks or more start on the same bank group).
+// 128-bit LDS read is served 16 lanes a cycle (256 bytes, 16 slots of 16
+// bytes): lanes l..l+7 with l+16..l+23, as the LDS counters of these tiles
+// show (four busy cycles a read and no conflicts with 128-byte rows, eight
+// with 512-byte rows and r & 7 below).  The MFMA operand reads put in such a
+// group rows r..r+7 (r a multiple of 8) at chunks c and c + 1, c even, so
+// those 16 accesses must fall on 16 different slots of a 256-byte line.
+// Rows of 8 chunks: two rows share a line, and c ^ (r & 7) puts chunks c and
+// c + 1 of a row on slots of opposite parity, each row pair on its own half.
+// Rows of 16 chunks or more all start a line: c ^ 2 (r & 7) spreads the
+// eight rows over the even slots, and c + 1 = c ^ 1 takes the odd ones.
+// (Rows shorter than 8 chunks: 8 / CPR rows share a 128-byte run.)
 template <int CPR>
 __device__ __forceinline__ int swz(int r, int c) {
-  if constexpr (CPR >= 8) return c ^ (r & 7);
+  if constexpr (CPR >= 16) return c ^ ((r & 7) << 1);
+  else if constexpr (CPR == 8) return c ^ (r & 7);
   else return c ^ ((r / (8 / CPR)) & (CPR - 1));
 }
 
