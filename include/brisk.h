@@ -11,7 +11,9 @@
  *   brisk_verify_accept  greedy verification: accepted-prefix length and the
  *                        correction token of each block.
  *
- * brisk_rerank_verify makes the last two in one call.
+ * brisk_rerank_verify makes the last two in one call; brisk_rerank_hoist and
+ * brisk_rerank_finish split the rerank at the candidates, so that its first
+ * part can overlap the LM-head pass.
  *
  * Conventions shared by every entry point
  *   - Every pointer argument is a DEVICE pointer owned by the caller, except
@@ -257,6 +259,34 @@ int brisk_verify_accept(const int32_t* proposal, const int32_t* verifier, int32_
  * Results equal the two calls made one after the other.
  */
 int brisk_rerank_verify(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                        const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                        const float* cand_logit, const int32_t* cand_id, const int32_t* verifier,
+                        int32_t B, int32_t L, int32_t K, int32_t d, int32_t V, int32_t* selected,
+                        float* refined, float* gamma, float* resid, int32_t* accept_len,
+                        int32_t* correction, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * brisk_rerank (or brisk_rerank_verify) in two parts, so that the first can
+ * run while the LM-head pass that makes the candidates streams (same section
+ * of the paper).  brisk_rerank_hoist queues the work that does not read the
+ * candidates: the projections P_h m_i, A_h h_c and A_e E(x_0), the sums of
+ * their split reductions, and their lifts into the step vectors together
+ * with the position and feature terms.  brisk_rerank_finish queues the rest
+ * on a workspace that a brisk_rerank_hoist call filled and nothing has
+ * written since: with verifier NULL it completes brisk_rerank, otherwise
+ * brisk_rerank_verify (then accept_len is required; correction is nullable).
+ *
+ * Both calls take brisk_rerank's arguments (brisk_rerank_hoist only those it
+ * reads) with the same c, hidden, ctx_hidden, anchor_tok, tok_embed, B, L,
+ * K, d, V and workspace, and the same limits and errors; the library does
+ * not check that the two calls agree.  The caller orders them: on one
+ * stream, or the finishing call's stream waits on an event recorded after
+ * the hoist.  The results are bitwise those of the single call.
+ */
+int brisk_rerank_hoist(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                       const int32_t* anchor_tok, const uint16_t* tok_embed, int32_t B, int32_t L,
+                       int32_t K, int32_t d, int32_t V, void* ws, size_t ws_bytes, void* stream);
+int brisk_rerank_finish(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
                         const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
                         const float* cand_logit, const int32_t* cand_id, const int32_t* verifier,
                         int32_t B, int32_t L, int32_t K, int32_t d, int32_t V, int32_t* selected,

@@ -29,7 +29,7 @@ from typing import Dict, Optional, Tuple
 
 import torch
 
-__all__ = ["BriskError", "Corrector", "propose_block", "propose_block_noalloc", "propose_lmhead", "propose_merge", "rerank", "rerank_verify", "verify_accept", "accept_profile",
+__all__ = ["BriskError", "Corrector", "propose_block", "propose_block_noalloc", "propose_lmhead", "propose_merge", "rerank", "rerank_verify", "rerank_hoist", "rerank_finish", "verify_accept", "accept_profile",
            "propose_verify", "verify_commit", "corrector_loss", "spec_verify",
            "lib", "LIB_PATH", "ABI_SYMBOLS", "propose_workspace_size", "rerank_workspace_size"]
 
@@ -38,6 +38,7 @@ ABI_SYMBOLS = ("brisk_status_str", "brisk_abi_version", "brisk_propose_workspace
                "brisk_propose_block", "brisk_propose_block_noalloc", "brisk_propose_lmhead",
                "brisk_propose_merge",
                "brisk_rerank_workspace_size", "brisk_rerank", "brisk_rerank_verify",
+               "brisk_rerank_hoist", "brisk_rerank_finish",
                "brisk_verify_accept", "brisk_propose_verify_workspace_size", "brisk_propose_verify",
                "brisk_verify_commit", "brisk_spec_verify_workspace_size", "brisk_spec_verify",
                "brisk_corrector_loss", "brisk_accept_profile_workspace_size",
@@ -100,6 +101,11 @@ def lib() -> ctypes.CDLL:
             L.brisk_rerank_verify.argtypes = [ctypes.POINTER(_CorrectorC), _p, _p, _p, _p, _p, _p, _p, _p,
                                               _i32, _i32, _i32, _i32, _i32, _p, _p, _p, _p, _p, _p,
                                               _p, _sz, _p]
+            L.brisk_rerank_hoist.restype = ctypes.c_int
+            L.brisk_rerank_hoist.argtypes = [ctypes.POINTER(_CorrectorC), _p, _p, _p, _p,
+                                             _i32, _i32, _i32, _i32, _i32, _p, _sz, _p]
+            L.brisk_rerank_finish.restype = ctypes.c_int
+            L.brisk_rerank_finish.argtypes = L.brisk_rerank_verify.argtypes
             L.brisk_verify_accept.restype = ctypes.c_int
             L.brisk_verify_accept.argtypes = [_p, _p, _i32, _i32, _p, _p, _p]
             L.brisk_propose_verify_workspace_size.restype = ctypes.c_int
@@ -456,6 +462,68 @@ def rerank_verify(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tenso
     _check(st, "brisk_rerank_verify")
     out["accept_len"] = accept_len
     out["correction"] = correction
+    return out
+
+
+def rerank_hoist(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anchor_tok: torch.Tensor,
+                 tok_embed: torch.Tensor, B: int, L: int, K: int, workspace: torch.Tensor, *,
+                 stream=None) -> None:
+    """The part of :func:`rerank` that does not read the candidates, queued on
+    ``stream`` into ``workspace`` (which :func:`rerank_finish` then completes);
+    it may run while the LM-head pass that makes the candidates streams."""
+    _dev_tensor(hidden, "hidden", torch.bfloat16, 2)
+    dev = hidden.device
+    rows, d = hidden.shape
+    if rows != B * L:
+        raise ValueError(f"hidden has {rows} rows, B*L = {B * L}")
+    if d != corr.d or corr.device != dev:
+        raise ValueError(f"the corrector was built for d = {corr.d} on {corr.device}, "
+                         f"the hidden states have d = {d} on {dev}")
+    _dev_tensor(ctx_hidden, "ctx_hidden", torch.bfloat16, shape=(B, d), device=dev)
+    _dev_tensor(anchor_tok, "anchor_tok", torch.int32, shape=(B,), device=dev)
+    _dev_tensor(tok_embed, "tok_embed", torch.bfloat16, 2, device=dev)
+    if tok_embed.shape[1] != d:
+        raise ValueError("hidden and tok_embed disagree on d")
+    V = tok_embed.shape[0]
+    need = rerank_workspace_size(corr, B, L, K)
+    st = lib().brisk_rerank_hoist(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
+                                  _ptr(anchor_tok), _ptr(tok_embed), B, L, K, d, V, _ptr(workspace),
+                                  _ws_bytes(workspace, dev, need), _stream_ptr(dev, stream))
+    _check(st, "brisk_rerank_hoist")
+
+
+def rerank_finish(corr: Corrector, hidden: torch.Tensor, ctx_hidden: torch.Tensor, anchor_tok: torch.Tensor,
+                  lm_head: torch.Tensor, tok_embed: torch.Tensor, cand_logit: torch.Tensor,
+                  cand_id: torch.Tensor, B: int, L: int, workspace: torch.Tensor, *,
+                  verifier: Optional[torch.Tensor] = None, want_scores: bool = False,
+                  selected: Optional[torch.Tensor] = None, refined: Optional[torch.Tensor] = None,
+                  gamma: Optional[torch.Tensor] = None, resid: Optional[torch.Tensor] = None,
+                  accept_len: Optional[torch.Tensor] = None, correction: Optional[torch.Tensor] = None,
+                  stream=None) -> Dict[str, torch.Tensor]:
+    """The rest of :func:`rerank` (``verifier`` None) or :func:`rerank_verify`
+    on a ``workspace`` that :func:`rerank_hoist` filled with the same inputs;
+    returns what that call returns."""
+    K, d, V, dev, ws, ws_n, out = _rerank_args(corr, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                                               cand_logit, cand_id, B, L, want_scores, selected, refined,
+                                               gamma, resid, workspace)
+    if verifier is not None:
+        _dev_tensor(verifier, "verifier", torch.int32, shape=(B, L), device=dev)
+        if accept_len is None:
+            accept_len = torch.empty(B, dtype=torch.int32, device=dev)
+        if correction is None:
+            correction = torch.empty(B, dtype=torch.int32, device=dev)
+        _dev_tensor(accept_len, "accept_len", torch.int32, shape=(B,), device=dev)
+        _dev_tensor(correction, "correction", torch.int32, shape=(B,), device=dev)
+    st = lib().brisk_rerank_finish(ctypes.byref(corr.c_struct), _ptr(hidden), _ptr(ctx_hidden),
+                                   _ptr(anchor_tok), _ptr(lm_head), _ptr(tok_embed), _ptr(cand_logit),
+                                   _ptr(cand_id), _ptr(verifier), B, L, K, d, V, _ptr(out["selected"]),
+                                   _ptr(out.get("refined")), _ptr(out.get("gamma")), _ptr(out.get("resid")),
+                                   _ptr(accept_len), _ptr(correction), _ptr(ws), ws_n,
+                                   _stream_ptr(dev, stream))
+    _check(st, "brisk_rerank_finish")
+    if verifier is not None:
+        out["accept_len"] = accept_len
+        out["correction"] = correction
     return out
 
 

@@ -10,7 +10,7 @@
 
 namespace {
 
-constexpr int kAbiVersion = 9;
+constexpr int kAbiVersion = 10;
 constexpr int32_t kMaxRows = 1 << 20;
 constexpr int32_t kMaxD = 65536;
 constexpr int32_t kMaxTableV = 1 << 24;
@@ -192,16 +192,17 @@ int brisk_rerank_workspace_size(const brisk_corrector* c, int32_t B, int32_t L, 
 
 namespace {
 
-int rerank_impl(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
-                const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
-                const float* cand_logit, const int32_t* cand_id, const int32_t* verifier, int32_t B,
-                int32_t L, int32_t K, int32_t d, int32_t V, int32_t* selected, float* refined,
-                float* gamma, float* resid, int32_t* accept_len, int32_t* correction, void* ws,
-                size_t ws_bytes, void* stream) {
+int rerank_impl(brisk::RerankPart part, const brisk_corrector* c, const uint16_t* hidden,
+                const uint16_t* ctx_hidden, const int32_t* anchor_tok, const uint16_t* lm_head,
+                const uint16_t* tok_embed, const float* cand_logit, const int32_t* cand_id,
+                const int32_t* verifier, int32_t B, int32_t L, int32_t K, int32_t d, int32_t V,
+                int32_t* selected, float* refined, float* gamma, float* resid, int32_t* accept_len,
+                int32_t* correction, void* ws, size_t ws_bytes, void* stream) {
   int st = corrector_check(c);
   if (st != BRISK_OK) return st;
-  if (!hidden || !ctx_hidden || !anchor_tok || !lm_head || !tok_embed || !cand_logit ||
-      !cand_id || !selected)
+  if (!hidden || !ctx_hidden || !anchor_tok || !tok_embed) return BRISK_ERR_NULL;
+  // the hoisted part reads no LM head, candidates or outputs
+  if (part != brisk::RerankPart::kHoist && (!lm_head || !cand_logit || !cand_id || !selected))
     return BRISK_ERR_NULL;
   st = rerank_shape_check(c, B, L, K);
   if (st != BRISK_OK) return st;
@@ -225,7 +226,7 @@ int rerank_impl(const brisk_corrector* c, const uint16_t* hidden, const uint16_t
   if (!aligned16(ws)) return BRISK_ERR_UNSUPPORTED;
   brisk::launch_rerank(*c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
                        B, L, K, d, V, selected, refined, gamma, resid, verifier, accept_len,
-                       correction, ws, static_cast<hipStream_t>(stream));
+                       correction, ws, static_cast<hipStream_t>(stream), part);
   return launch_status();
 }
 
@@ -236,9 +237,9 @@ int brisk_rerank(const brisk_corrector* c, const uint16_t* hidden, const uint16_
                  const float* cand_logit, const int32_t* cand_id, int32_t B, int32_t L, int32_t K,
                  int32_t d, int32_t V, int32_t* selected, float* refined, float* gamma,
                  float* resid, void* ws, size_t ws_bytes, void* stream) {
-  return rerank_impl(c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
-                     nullptr, B, L, K, d, V, selected, refined, gamma, resid, nullptr, nullptr, ws,
-                     ws_bytes, stream);
+  return rerank_impl(brisk::RerankPart::kAll, c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                     cand_logit, cand_id, nullptr, B, L, K, d, V, selected, refined, gamma, resid,
+                     nullptr, nullptr, ws, ws_bytes, stream);
 }
 
 int brisk_rerank_verify(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
@@ -249,9 +250,31 @@ int brisk_rerank_verify(const brisk_corrector* c, const uint16_t* hidden, const 
                         int32_t* correction, void* ws, size_t ws_bytes, void* stream) {
   if (!verifier || !accept_len) return BRISK_ERR_NULL;
   if (!aligned4(verifier) || !aligned4(accept_len) || !aligned4(correction)) return BRISK_ERR_UNSUPPORTED;
-  return rerank_impl(c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed, cand_logit, cand_id,
-                     verifier, B, L, K, d, V, selected, refined, gamma, resid, accept_len, correction,
-                     ws, ws_bytes, stream);
+  return rerank_impl(brisk::RerankPart::kAll, c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                     cand_logit, cand_id, verifier, B, L, K, d, V, selected, refined, gamma, resid,
+                     accept_len, correction, ws, ws_bytes, stream);
+}
+
+int brisk_rerank_hoist(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                       const int32_t* anchor_tok, const uint16_t* tok_embed, int32_t B, int32_t L,
+                       int32_t K, int32_t d, int32_t V, void* ws, size_t ws_bytes, void* stream) {
+  return rerank_impl(brisk::RerankPart::kHoist, c, hidden, ctx_hidden, anchor_tok, nullptr, tok_embed,
+                     nullptr, nullptr, nullptr, B, L, K, d, V, nullptr, nullptr, nullptr, nullptr,
+                     nullptr, nullptr, ws, ws_bytes, stream);
+}
+
+int brisk_rerank_finish(const brisk_corrector* c, const uint16_t* hidden, const uint16_t* ctx_hidden,
+                        const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
+                        const float* cand_logit, const int32_t* cand_id, const int32_t* verifier,
+                        int32_t B, int32_t L, int32_t K, int32_t d, int32_t V, int32_t* selected,
+                        float* refined, float* gamma, float* resid, int32_t* accept_len,
+                        int32_t* correction, void* ws, size_t ws_bytes, void* stream) {
+  if (verifier && !accept_len) return BRISK_ERR_NULL;
+  if (!aligned4(verifier) || !aligned4(accept_len) || !aligned4(correction)) return BRISK_ERR_UNSUPPORTED;
+  return rerank_impl(brisk::RerankPart::kFinish, c, hidden, ctx_hidden, anchor_tok, lm_head, tok_embed,
+                     cand_logit, cand_id, verifier, B, L, K, d, V, selected, refined, gamma, resid,
+                     verifier ? accept_len : nullptr, verifier ? correction : nullptr, ws, ws_bytes,
+                     stream);
 }
 
 int brisk_corrector_tables_size(const brisk_corrector* c, int32_t V, size_t* table_bytes, size_t* ws_bytes) {

@@ -1337,8 +1337,15 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
                    const float* cand_logit, const int32_t* cand_id, int B, int L, int K, int d,
                    int V, int32_t* selected, float* refined, float* gamma, float* resid,
                    const int32_t* verifier, int32_t* accept_len, int32_t* correction, void* ws,
-                   hipStream_t s) {
+                   hipStream_t s, RerankPart part) {
   const bool tab = c.tables != nullptr;
+  // The hoisted part: the hidden-state, context and A_e anchor projections,
+  // the sums of their split slices and their lifts (with the feature maps).
+  // The rest reads candidates, or (without the tables) shares the PE array
+  // and its slice sum with them: the candidate and anchor P_e projections,
+  // the W_c projections, the cross logits, their lifts, the table rows, the
+  // scan and the verification.
+  const bool hoist = part != RerankPart::kFinish, finish = part != RerankPart::kHoist;
   const Layout lay = rerank_layout(c, B, L, K, tab);
   char* base = static_cast<char*>(ws);
   auto F = [&](size_t off) { return reinterpret_cast<float*>(base + off); };
@@ -1354,15 +1361,17 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   // With the per-token tables, every per-candidate and per-anchor lift is a
   // table row: the projections of candidates and anchors are not computed.
   const int n_cand = tab ? 0 : NC, n_anch = tab ? 0 : B;
+  const int fc = finish ? n_cand : 0, fa = finish ? n_anch : 0;  // rows of the finishing jobs
+  const int hr = hoist ? rows : 0, hb = hoist ? B : 0;             // and of the hoisted ones
   ProjJobs pj{};
   pj.d = d;
   pj.splits = S;
-  pj.job[0] = ProjJob{tok_embed, cand_id, n_cand, c.d_tproj, V, c.P_e, F(lay.PE), sPE};
-  pj.job[1] = ProjJob{tok_embed, anchor_tok, n_anch, c.d_tproj, V, c.P_e, F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj, sPE};
-  pj.job[2] = ProjJob{lm_head, cand_id, n_cand, c.rank, V, c.W_c, F(lay.PC), sPC};
-  pj.job[3] = ProjJob{hidden, nullptr, rows, c.d_hproj, rows, c.P_h, F(lay.PH), sPH};
-  pj.job[4] = ProjJob{ctx_hidden, nullptr, B, ds, B, c.A_h, F(lay.U0), sU0};
-  pj.job[5] = ProjJob{tok_embed, anchor_tok, B, ds, V, c.A_e, F(lay.U0) + static_cast<size_t>(B) * ds, sU0};
+  pj.job[0] = ProjJob{tok_embed, cand_id, fc, c.d_tproj, V, c.P_e, F(lay.PE), sPE};
+  pj.job[1] = ProjJob{tok_embed, anchor_tok, fa, c.d_tproj, V, c.P_e, F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj, sPE};
+  pj.job[2] = ProjJob{lm_head, cand_id, fc, c.rank, V, c.W_c, F(lay.PC), sPC};
+  pj.job[3] = ProjJob{hidden, nullptr, hr, c.d_hproj, rows, c.P_h, F(lay.PH), sPH};
+  pj.job[4] = ProjJob{ctx_hidden, nullptr, hb, ds, B, c.A_h, F(lay.U0), sU0};
+  pj.job[5] = ProjJob{tok_embed, anchor_tok, hb, ds, V, c.A_e, F(lay.U0) + static_cast<size_t>(B) * ds, sU0};
   // unsplit (batched) shapes take 128-wide output tiles
   const int bj = S == 1 ? 128 : 64;
   int max_tiles = 0;
@@ -1371,30 +1380,32 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
     max_tiles = t > max_tiles ? t : max_tiles;
   }
   const int group = NC >= 4096 ? 8 : 1;
-  pj.cross = CrossJob{lm_head, hidden, cand_id, anchor_tok, B, L, K, V, F(lay.X), group};
+  // (no sequences: no cross logits in the hoisted part)
+  pj.cross = CrossJob{lm_head, hidden, cand_id, anchor_tok, finish ? B : 0, L, K, V, F(lay.X), group};
   // the cross-logit row needs a wavefront per row and group of candidates,
   // and one per anchor, four to a workgroup (each loops over more when the
   // grid is capped at about 4096 workgroups)
-  const int cross_items = rows * ((K + group - 1) / group) + B;
+  const int cross_items = finish ? rows * ((K + group - 1) / group) + B : 0;
   const int cross_x = std::min(((cross_items + 3) / 4 + S - 1) / S, (4096 + S - 1) / S);
   const int gx = std::max(max_tiles, cross_x);
-  if (bj == 128)
-    hipLaunchKernelGGL(gather_proj_kernel<128>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
-  else
-    hipLaunchKernelGGL(gather_proj_kernel<64>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
+  if (gx > 0) {
+    if (bj == 128)
+      hipLaunchKernelGGL(gather_proj_kernel<128>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
+    else
+      hipLaunchKernelGGL(gather_proj_kernel<64>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
+  }
 
   if (S > 1) {
     SliceArrs sl{};
     sl.splits = S;
-    sl.arr[0] = SliceArr{F(lay.PE), tab ? 0 : sPE, sPE};
-    sl.arr[1] = SliceArr{F(lay.PC), tab ? 0 : sPC, sPC};
-    sl.arr[2] = SliceArr{F(lay.PH), sPH, sPH};
-    sl.arr[3] = SliceArr{F(lay.U0), sU0, sU0};
-    size_t mx = sPE > sPC ? sPE : sPC;
-    mx = mx > sPH ? mx : sPH;
-    mx = mx > sU0 ? mx : sU0;
+    sl.arr[0] = SliceArr{F(lay.PE), tab || !finish ? 0 : sPE, sPE};
+    sl.arr[1] = SliceArr{F(lay.PC), tab || !finish ? 0 : sPC, sPC};
+    sl.arr[2] = SliceArr{F(lay.PH), hoist ? sPH : 0, sPH};
+    sl.arr[3] = SliceArr{F(lay.U0), hoist ? sU0 : 0, sU0};
+    size_t mx = 0;
+    for (int a = 0; a < kMaxSliceArrs; ++a) mx = sl.arr[a].n > mx ? sl.arr[a].n : mx;
     const int blocks = static_cast<int>((mx / 4 + 255) / 256);
-    hipLaunchKernelGGL(slice_sum_kernel, dim3(blocks, kMaxSliceArrs), dim3(256), 0, s, sl);
+    if (blocks > 0) hipLaunchKernelGGL(slice_sum_kernel, dim3(blocks, kMaxSliceArrs), dim3(256), 0, s, sl);
   }
 
   // Step blocks: row r holds F = 2 + 3K vectors [AZ, AH, EH_k, TZ_k, TH_k].
@@ -1425,24 +1436,28 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   const LiftTerm posz = term(c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_z + pos_off, d_in, 1);
   const LiftTerm posh = term(c.pos_emb, 1, c.d_pos, 1, L, c.d_pos, c.W_h + pos_off, d_in, 1);
   const size_t vds = static_cast<size_t>(ds);
-  lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, n_cand, SB + (2 + K) * vsz, K, blk, vsz};
-  lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, n_cand, SB + (2 + 2 * K) * vsz, K, blk, vsz};
-  lj.job[2] = LiftJob{{fterm(F(lay.PC), c.rank, c.W_s, 1, ds), none}, n_cand, SB + 2 * vsz, K, blk, vsz};
-  lj.job[3] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_z, d_in, 1), posz}, rows, SB, 1, blk, vsz};
-  lj.job[4] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_h, d_in, 1), posh}, rows, SB + vsz, 1, blk, vsz};
-  lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, n_anch, F(lay.TZA), 1, vds, vds};
-  lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, n_anch, F(lay.THA), 1, vds, vds};
+  lj.job[0] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_z + tp_off, d_in, 1), none}, fc, SB + (2 + K) * vsz, K, blk, vsz};
+  lj.job[1] = LiftJob{{fterm(F(lay.PE), c.d_tproj, c.W_h + tp_off, d_in, 1), none}, fc, SB + (2 + 2 * K) * vsz, K, blk, vsz};
+  lj.job[2] = LiftJob{{fterm(F(lay.PC), c.rank, c.W_s, 1, ds), none}, fc, SB + 2 * vsz, K, blk, vsz};
+  lj.job[3] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_z, d_in, 1), posz}, hr, SB, 1, blk, vsz};
+  lj.job[4] = LiftJob{{fterm(F(lay.PH), c.d_hproj, c.W_h, d_in, 1), posh}, hr, SB + vsz, 1, blk, vsz};
+  lj.job[5] = LiftJob{{fterm(PEa, c.d_tproj, c.W_z + tp_off, d_in, 1), none}, fa, F(lay.TZA), 1, vds, vds};
+  lj.job[6] = LiftJob{{fterm(PEa, c.d_tproj, c.W_h + tp_off, d_in, 1), none}, fa, F(lay.THA), 1, vds, vds};
   // feature maps W_z[:, feat] P_phi and W_h[:, feat] P_phi as [5, ds]: input row f is column f of P_phi
-  lj.job[7] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1), none}, 5, F(lay.FZ), 1, vds, vds};
-  lj.job[8] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1), none}, 5, F(lay.FH), 1, vds, vds};
+  lj.job[7] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_z + feat_off, d_in, 1), none}, hoist ? 5 : 0, F(lay.FZ), 1, vds, vds};
+  lj.job[8] = LiftJob{{term(c.P_phi, 1, 1, 5, 0, c.d_feat, c.W_h + feat_off, d_in, 1), none}, hoist ? 5 : 0, F(lay.FH), 1, vds, vds};
   const int lift_cols = static_cast<int>(vsz > vds ? vsz : vds);
   int lift_rows = 0;
   for (int j = 0; j < kMaxLiftJobs; ++j) lift_rows = lj.job[j].n > lift_rows ? lj.job[j].n : lift_rows;
   const dim3 lift_grid((lift_rows + LT_BN - 1) / LT_BN, (lift_cols + LT_BJ - 1) / LT_BJ, kMaxLiftJobs);
   // the candidate jobs' tiles: more than two per compute unit -> one buffer
+  // (the same choice in both parts of a split rerank)
   const bool many_tiles = 3 * ((n_cand + LT_BN - 1) / LT_BN) * ((ds + LT_BJ - 1) / LT_BJ) > 512;
-  if (many_tiles) hipLaunchKernelGGL(lift_kernel<1>, lift_grid, dim3(256), 0, s, lj);
-  else hipLaunchKernelGGL(lift_kernel<2>, lift_grid, dim3(256), 0, s, lj);
+  if (lift_rows > 0) {
+    if (many_tiles) hipLaunchKernelGGL(lift_kernel<1>, lift_grid, dim3(256), 0, s, lj);
+    else hipLaunchKernelGGL(lift_kernel<2>, lift_grid, dim3(256), 0, s, lj);
+  }
+  if (!finish) return;
   const bool pc = ds <= 256 && K <= 16;  // the single-wave scan, which can verify in the same pass
   // Who brings the table rows to the scan.  The single-wave scan can gather
   // them itself (its copy wave issues each row's copies three rows ahead), but

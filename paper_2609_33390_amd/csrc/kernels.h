@@ -42,12 +42,19 @@ void launch_spec_verify(const uint16_t* Hv, const uint16_t* W, int B, int L, int
 
 // ---- rerank: hoisted projections + sequential scan -------------------------
 size_t rerank_workspace_bytes(const brisk_corrector& c, int B, int L, int K);
+// What one launch_rerank call queues: the whole rerank; only the work that
+// does not read the candidates (projections of the hidden states, the
+// context and the anchors' embeddings, their lifts), which may run while the
+// LM-head pass that makes the candidates streams; or only the rest, on a
+// workspace the hoisted part filled.  Split or not, the results are the same
+// bits.
+enum class RerankPart { kAll, kHoist, kFinish };
 void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint16_t* ctx_hidden,
                    const int32_t* anchor_tok, const uint16_t* lm_head, const uint16_t* tok_embed,
                    const float* cand_logit, const int32_t* cand_id, int B, int L, int K, int d,
                    int V, int32_t* selected, float* refined, float* gamma, float* resid,
                    const int32_t* verifier, int32_t* accept_len, int32_t* correction, void* ws,
-                   hipStream_t s);
+                   hipStream_t s, RerankPart part = RerankPart::kAll);
 
 // Per-token tables [EH; TZ; TH], each [V][step vector stride] fp32, and the
 // scratch their preparation needs.

@@ -984,6 +984,13 @@ using MidRows = TileCfg<256, 64, 4, 1, 64, 3>;      // <= 64 rows
 using LargeRows = TileCfg<256, 256, 4, 2, 64, 2>;   // many rows: MFMA bound
 
 constexpr int kTargetWorkgroups = 256;  // one persistent workgroup per compute unit
+// The plain pass at 32 rows or fewer streams lm_head as fast from 224
+// compute units (28 per XCD) as from 256 (169-170 against 172 us at 32
+// rows; 192 units: 186 us) and leaves 32 free for work on another stream
+// (brisk_rerank_hoist): a whole 44 us rerank beside it ends 8 us after the
+// pass's 170, where beside a 256-unit pass the two took 229 us.  The
+// sampling pass keeps every unit (it is 1-7 us slower on 224).
+constexpr int kSmallRowsWorkgroups = 224;
 
 struct Plan {
   int cfg;  // 0 small, 1 mid, 2 large
@@ -992,12 +999,12 @@ struct Plan {
 };
 
 template <class C>
-Plan make_plan_for(int cfg, int rows, int V, int K) {
+Plan make_plan_for(int cfg, int rows, int V, int K, int target = kTargetWorkgroups) {
   Plan p{};
   p.cfg = cfg;
   p.n_rtiles = (rows + C::BR - 1) / C::BR;
   p.n_vtiles = (V + C::BV - 1) / C::BV;
-  int want = kTargetWorkgroups / p.n_rtiles;
+  int want = target / p.n_rtiles;
   want = want < 1 ? 1 : (want > p.n_vtiles ? p.n_vtiles : want);
   p.tiles_per_group = (p.n_vtiles + want - 1) / want;
   p.n_groups = (p.n_vtiles + p.tiles_per_group - 1) / p.tiles_per_group;
@@ -1005,7 +1012,7 @@ Plan make_plan_for(int cfg, int rows, int V, int K) {
   // idle, cut the vocabulary into one equal share per compute unit instead
   // (the partly masked last tile costs MFMA time, which these shapes have
   // to spare, but no memory traffic).
-  const int want_all = kTargetWorkgroups / p.n_rtiles < 1 ? 1 : kTargetWorkgroups / p.n_rtiles;
+  const int want_all = target / p.n_rtiles < 1 ? 1 : target / p.n_rtiles;
   p.even = 0;
   if (kEvenShares && cfg != 2 && p.n_groups < want_all && V / want_all >= C::BV / 2) {
     p.even = 1;
@@ -1022,8 +1029,8 @@ Plan make_plan_for(int cfg, int rows, int V, int K) {
   return p;
 }
 
-Plan make_plan(int rows, int V, int K) {
-  if (rows <= 32) return make_plan_for<SmallRows>(0, rows, V, K);
+Plan make_plan(int rows, int V, int K, bool sample = false) {
+  if (rows <= 32) return make_plan_for<SmallRows>(0, rows, V, K, sample ? kTargetWorkgroups : kSmallRowsWorkgroups);
   if (rows <= 64) return make_plan_for<MidRows>(1, rows, V, K);
   return make_plan_for<LargeRows>(2, rows, V, K);
 }
@@ -1275,7 +1282,7 @@ struct SpecLayout {
 SpecLayout spec_layout(int B, int L, int V, int K) {
   SpecLayout l{};
   const int rows = B * L;
-  l.plan = make_plan(rows, V, 1);  // the best non-candidate key per row
+  l.plan = make_plan(rows, V, 1, true);  // the best non-candidate key per row
   auto up = [](size_t n) { return (n + 255) / 256 * 256; };
   l.keys = 0;
   l.lse = up(static_cast<size_t>(rows) * l.plan.n_parts * l.plan.KP * sizeof(uint64_t));

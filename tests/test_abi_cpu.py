@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_status_strings_and_version():
     L = brisk.lib()
-    assert L.brisk_abi_version() == 9
+    assert L.brisk_abi_version() == 10
     for st in (OK, ENULL, ESHAPE, EUNSUP, EWS, -5, -6):
         assert L.brisk_status_str(st).decode() != "unknown status"
         assert L.brisk_status_str(st).decode()
@@ -151,6 +151,49 @@ def _rerank_verify(c=None, **kw):
 ])
 def test_rerank_verify_validation(ckw, kw, want):
     assert _rerank_verify(_corr(**ckw), **kw) == want
+
+
+def _rerank_hoist(c=None, **kw):
+    a = dict(hidden=FAKE, ctx=FAKE, anchor=FAKE, E=FAKE, B=1, L=32, K=8, d=4096, V=126464, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    c = _corr() if c is None else c
+    return brisk.lib().brisk_rerank_hoist(ctypes.byref(c), a["hidden"], a["ctx"], a["anchor"], a["E"], a["B"],
+                                          a["L"], a["K"], a["d"], a["V"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("ckw,kw,want", [
+    (dict(A_h=None), {}, ENULL), ({}, dict(hidden=None), ENULL), ({}, dict(ctx=None), ENULL),
+    ({}, dict(anchor=None), ENULL), ({}, dict(E=None), ENULL),
+    ({}, dict(K=3), ESHAPE), ({}, dict(L=33), ESHAPE), ({}, dict(B=0), ESHAPE), (dict(d_state=513), {}, ESHAPE),
+    ({}, dict(d=4092), EUNSUP), ({}, dict(E=MISALIGNED), EUNSUP), ({}, dict(ws=MISALIGNED, ws_bytes=1 << 40), EUNSUP),
+    ({}, dict(ws_bytes=16), EWS), ({}, dict(ws=None, ws_bytes=1 << 40), EWS),
+])
+def test_rerank_hoist_validation(ckw, kw, want):
+    # the hoisted part reads no LM head or candidates: the call gets none
+    assert _rerank_hoist(_corr(**ckw), **kw) == want
+
+
+def _rerank_finish(c=None, **kw):
+    a = dict(hidden=FAKE, ctx=FAKE, anchor=FAKE, W=FAKE, E=FAKE, cl=FAKE, ci=FAKE, ver=None, B=1, L=32, K=8,
+             d=4096, V=126464, sel=FAKE, ref=None, gam=None, res=None, acc=None, cor=None, ws=FAKE, ws_bytes=0)
+    a.update(kw)
+    c = _corr() if c is None else c
+    return brisk.lib().brisk_rerank_finish(ctypes.byref(c), a["hidden"], a["ctx"], a["anchor"], a["W"], a["E"],
+                                           a["cl"], a["ci"], a["ver"], a["B"], a["L"], a["K"], a["d"], a["V"],
+                                           a["sel"], a["ref"], a["gam"], a["res"], a["acc"], a["cor"], a["ws"],
+                                           a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("ckw,kw,want", [
+    ({}, dict(W=None), ENULL), ({}, dict(cl=None), ENULL), ({}, dict(ci=None), ENULL), ({}, dict(sel=None), ENULL),
+    ({}, dict(ver=FAKE), ENULL),                      # a verifier needs accept_len
+    (dict(W_s=None), {}, ENULL),
+    ({}, dict(ver=FAKE, acc=MISALIGNED), EUNSUP), ({}, dict(cor=MISALIGNED), EUNSUP),
+    ({}, dict(K=65), ESHAPE), ({}, dict(L=33), ESHAPE),
+    ({}, dict(ws_bytes=16), EWS), ({}, dict(ver=FAKE, acc=FAKE, ws_bytes=16), EWS),
+])
+def test_rerank_finish_validation(ckw, kw, want):
+    assert _rerank_finish(_corr(**ckw), **kw) == want
 
 
 def test_rerank_workspace_size_query():
