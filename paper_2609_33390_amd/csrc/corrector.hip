@@ -83,8 +83,12 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 c, float s) {
   return s;
 }
 
+// G candidates a wavefront at most, U 512-element chunks of each operand in
+// flight per lane.  One candidate a wavefront takes eight chunks, so a 4096-
+// long dot is one round of loads instead of four (the accumulation order
+// over k is the same).
+template <int G, int U>
 __device__ void cross_dots(const CrossJob& cj, int d) {
-  constexpr int G = 8, U = 2;
   const int lane = threadIdx.x & 63;
   const int rows = cj.B * cj.L, NC = rows * cj.K;
   const int g = cj.group;
@@ -152,7 +156,8 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   constexpr int WJ = BJ / 2, TJ = WJ / 16;  // a wave's outputs and 16-wide fragments
   const int d = jobs.d;
   if (blockIdx.y == kMaxProjJobs) {
-    cross_dots(jobs.cross, d);
+    if (jobs.cross.group == 1) cross_dots<1, 8>(jobs.cross, d);
+    else cross_dots<8, 2>(jobs.cross, d);
     return;
   }
   const ProjJob& jb = jobs.job[blockIdx.y];
