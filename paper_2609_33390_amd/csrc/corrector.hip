@@ -51,9 +51,59 @@ struct CrossJob {
   float* X;
   int group;  // candidates per wavefront, 1..8
 };
+// Table rows into the step blocks (with the per-token tables): for every
+// candidate its EH, TZ and TH rows, for every anchor its TZ and TH rows; one
+// wavefront per row, rows first..n_vec-1 in steps of `step`.
+struct FillArgs {
+  const float* tables;   // [3][V][vs]: EH, TZ, TH
+  const int32_t* cand_id;
+  const int32_t* anchor;
+  float* SB;             // [rows][2 + 3K][vs]
+  float* TZA;            // [B][ds]
+  float* THA;
+  int rows, K, B, V, ds, vs;  // rows = B = 0: nothing to copy
+};
+
+__device__ void fill_rows(const FillArgs& a, int first, int step) {
+  const int lane = threadIdx.x & 63;
+  const int n_cand = a.rows * 3 * a.K;
+  for (int n = first; n < n_cand + 2 * a.B; n += step) {
+    const float* src;
+    float* dst;
+    int len;
+    if (n < n_cand) {
+      const int r = n / (3 * a.K), f = n % (3 * a.K), kind = f / a.K, k = f % a.K;
+      const int v = clamp_id(a.cand_id[static_cast<size_t>(r) * a.K + k], a.V);
+      src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
+      dst = a.SB + (static_cast<size_t>(r) * (2 + 3 * a.K) + 2 + f) * a.vs;
+      len = a.vs;
+    } else {
+      const int m = n - n_cand, b = m % a.B, kind = 1 + m / a.B;  // TZ, then TH
+      const int v = clamp_id(a.anchor[b], a.V);
+      src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
+      dst = (kind == 1 ? a.TZA : a.THA) + static_cast<size_t>(b) * a.ds;
+      len = a.ds;
+    }
+    if ((len & 3) == 0) {
+      for (int e = lane * 4; e < len; e += 256)
+        *reinterpret_cast<float4*>(dst + e) = *reinterpret_cast<const float4*>(src + e);
+    } else {
+      for (int e = lane; e < len; e += 64) dst[e] = src[e];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void fill_kernel(FillArgs a) {
+  fill_rows(a, blockIdx.x * 4 + (threadIdx.x >> 6), gridDim.x * 4);
+}
+
+// One launch: the projection jobs (grid rows 0..kMaxProjJobs-1), the cross
+// logits (row kMaxProjJobs) and the table rows (row kMaxProjJobs + 1), which
+// all read nothing the others write.
 struct ProjJobs {
   ProjJob job[kMaxProjJobs];
   CrossJob cross;
+  FillArgs fill;
   int d, splits;
 };
 
@@ -158,6 +208,10 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   if (blockIdx.y == kMaxProjJobs) {
     if (jobs.cross.group == 1) cross_dots<1, 8>(jobs.cross, d);
     else cross_dots<8, 2>(jobs.cross, d);
+    return;
+  }
+  if (blockIdx.y == kMaxProjJobs + 1) {
+    fill_rows(jobs.fill, (blockIdx.z * gridDim.x + blockIdx.x) * 4 + (threadIdx.x >> 6), gridDim.x * gridDim.z * 4);
     return;
   }
   const ProjJob& jb = jobs.job[blockIdx.y];
@@ -1226,45 +1280,6 @@ __global__ __launch_bounds__(128) void scan_pc_kernel(ScanArgs a, const int32_t*
 // and TH tables, and the anchor lifts TZA, THA are rows x_0 of TZ and TH.
 // One wavefront copies one vector, 16 bytes per lane.
 // ---------------------------------------------------------------------------
-struct FillArgs {
-  const float* tables;   // [3][V][vs]: EH, TZ, TH
-  const int32_t* cand_id;
-  const int32_t* anchor;
-  float* SB;             // [rows][2 + 3K][vs]
-  float* TZA;            // [B][ds]
-  float* THA;
-  int rows, K, B, V, ds, vs;
-};
-
-__global__ __launch_bounds__(256) void fill_kernel(FillArgs a) {
-  const int lane = threadIdx.x & 63;
-  const int n_cand = a.rows * 3 * a.K;
-  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (n >= n_cand + 2 * a.B) return;
-  const float* src;
-  float* dst;
-  int len;
-  if (n < n_cand) {
-    const int r = n / (3 * a.K), f = n % (3 * a.K), kind = f / a.K, k = f % a.K;
-    const int v = clamp_id(a.cand_id[static_cast<size_t>(r) * a.K + k], a.V);
-    src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
-    dst = a.SB + (static_cast<size_t>(r) * (2 + 3 * a.K) + 2 + f) * a.vs;
-    len = a.vs;
-  } else {
-    const int m = n - n_cand, b = m % a.B, kind = 1 + m / a.B;  // TZ, then TH
-    const int v = clamp_id(a.anchor[b], a.V);
-    src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
-    dst = (kind == 1 ? a.TZA : a.THA) + static_cast<size_t>(b) * a.ds;
-    len = a.ds;
-  }
-  if ((len & 3) == 0) {
-    for (int e = lane * 4; e < len; e += 256)
-      *reinterpret_cast<float4*>(dst + e) = *reinterpret_cast<const float4*>(src + e);
-  } else {
-    for (int e = lane; e < len; e += 64) dst[e] = src[e];
-  }
-}
-
 // Vector stride of the step blocks: one 256-float vector per field when the
 // state fits (the single-wave scan copies whole 1 KiB vectors), else d_state.
 size_t step_vec_stride(int ds) { return ds <= 256 ? 256 : static_cast<size_t>(ds); }
@@ -1392,13 +1407,41 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   // grid is capped at about 4096 workgroups)
   const int cross_items = finish ? rows * ((K + group - 1) / group) + B : 0;
   const int cross_x = std::min(((cross_items + 3) / 4 + S - 1) / S, (4096 + S - 1) / S);
-  const int gx = std::max(max_tiles, cross_x);
+  const bool pc = ds <= 256 && K <= 16;  // the single-wave scan, which can verify in the same pass
+  // Who brings the table rows to the scan.  The single-wave scan can gather
+  // them itself (its copy wave issues each row's copies three rows ahead), but
+  // random 1 KiB reads from the tables outlast that lead: at 32 rows the scan
+  // took 40 instead of 23 us, with 16 keys (two rows of lead) 72 instead of
+  // 36 us.  Copying the rows into the step blocks first is a parallel,
+  // bandwidth-bound pass whose cost grows with the batch (5 us at 32 rows,
+  // 17 us at 2048, 32 us at 4096), against a latency the gathering scan pays
+  // once per step whatever the batch: the whole rerank took 89.5 against
+  // 76.3 us with gathering at 64 x 32 rows, and 165 against 140 us at
+  // 256 x 16, so the scan gathers from 64 sequences on.
+  const bool scan_gathers = tab && pc && K <= 8 && B >= 64;
+  // Without it the scan reads whole step blocks and the table rows are
+  // copied in, a wavefront per row.  Up to 4096 rows (4 MiB) the projection
+  // launch copies them, two rows a wavefront at most, which saves a launch
+  // (32 rows: 2.5 us of a rerank's 43); more would stretch that launch
+  // (512 x 16 rows: 24 us against 15 + 8 us for two launches).
+  const size_t vsz = step_vec_stride(ds);
+  float* SB = F(lay.SB);
+  const bool fill = finish && tab && !scan_gathers;
+  const int n_vec = fill ? rows * 3 * K + 2 * B : 0;
+  const bool fill_here = fill && n_vec <= 4096;
+  const FillArgs fargs{c.tables, cand_id, anchor_tok, SB, F(lay.TZA), F(lay.THA), fill ? rows : 0, K,
+                       fill ? B : 0, V, ds, static_cast<int>(vsz)};
+  if (fill_here) pj.fill = fargs;
+  const int fill_x = fill_here ? std::min(((n_vec + 7) / 8 + S - 1) / S, (4096 + S - 1) / S) : 0;
+  const int gx = std::max(max_tiles, std::max(cross_x, fill_x));
+  const int gy = kMaxProjJobs + (fill_here ? 2 : 1);  // the table-row row only when it copies
   if (gx > 0) {
     if (bj == 128)
-      hipLaunchKernelGGL(gather_proj_kernel<128>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
+      hipLaunchKernelGGL(gather_proj_kernel<128>, dim3(gx, gy, S), dim3(256), 0, s, pj);
     else
-      hipLaunchKernelGGL(gather_proj_kernel<64>, dim3(gx, kMaxProjJobs + 1, S), dim3(256), 0, s, pj);
+      hipLaunchKernelGGL(gather_proj_kernel<64>, dim3(gx, gy, S), dim3(256), 0, s, pj);
   }
+  if (fill && !fill_here) hipLaunchKernelGGL(fill_kernel, dim3((n_vec + 3) / 4), dim3(256), 0, s, fargs);
 
   if (S > 1) {
     SliceArrs sl{};
@@ -1415,9 +1458,7 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
 
   // Step blocks: row r holds F = 2 + 3K vectors [AZ, AH, EH_k, TZ_k, TH_k].
   const int FB = 2 + 3 * K;
-  const size_t vsz = step_vec_stride(ds);
   const size_t blk = static_cast<size_t>(FB) * vsz;
-  float* SB = F(lay.SB);
   LiftJobs lj{};
   lj.ds = ds;
   const float* PEa = F(lay.PE) + static_cast<size_t>(NC) * c.d_tproj;
@@ -1463,25 +1504,6 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
     else hipLaunchKernelGGL(lift_kernel<2>, lift_grid, dim3(256), 0, s, lj);
   }
   if (!finish) return;
-  const bool pc = ds <= 256 && K <= 16;  // the single-wave scan, which can verify in the same pass
-  // Who brings the table rows to the scan.  The single-wave scan can gather
-  // them itself (its copy wave issues each row's copies three rows ahead), but
-  // random 1 KiB reads from the tables outlast that lead: at 32 rows the scan
-  // took 40 instead of 23 us, with 16 keys (two rows of lead) 72 instead of
-  // 36 us.  Copying the rows into the step blocks first is a parallel,
-  // bandwidth-bound pass whose cost grows with the batch (5 us at 32 rows,
-  // 17 us at 2048, 32 us at 4096), against a latency the gathering scan pays
-  // once per step whatever the batch: the whole rerank took 89.5 against
-  // 76.3 us with gathering at 64 x 32 rows, and 165 against 140 us at
-  // 256 x 16, so the scan gathers from 64 sequences on.
-  const bool scan_gathers = tab && pc && K <= 8 && B >= 64;
-  if (tab && !scan_gathers) {
-    // the scan reads whole step blocks: copy the table rows in
-    const FillArgs fa{c.tables, cand_id, anchor_tok, SB, F(lay.TZA), F(lay.THA), rows, K, B, V, ds,
-                      static_cast<int>(vsz)};
-    const int n_vec = rows * 3 * K + 2 * B;
-    hipLaunchKernelGGL(fill_kernel, dim3((n_vec + 3) / 4), dim3(256), 0, s, fa);
-  }
 
   ScanArgs sa{};
   sa.B = B; sa.L = L; sa.K = K; sa.ds = ds; sa.vs = static_cast<int>(vsz);
