@@ -607,6 +607,12 @@ __global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA /
         // lane l holds, for position wr*WR + y*16 + l%16, the logits of
         // vocabulary rows wv*WV + x*16 + 4*(l/16) + q of the tile
         uint64_t* const sq = reinterpret_cast<uint64_t*>(sE);
+        // Queue entry i of position p: the slot XORed with the position, so
+        // that the lanes of 16 positions storing (or the list owners
+        // reading) the same entry index hit different banks (rows of the
+        // queue are 256 bytes apart).
+        static_assert((C::QCAP & (C::QCAP - 1)) == 0, "queue slots");
+        auto qslot = [](int p, int i) { return p * C::QCAP + (i ^ (p & (C::QCAP - 1))); };
         if (seed) {
           // Seed from the tile itself: each of the 16 lanes that hold a
           // position's 256 logits offers its M largest, and the KP-th
@@ -691,27 +697,31 @@ __global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA /
           last[y] = li;
           mx[y] = m;
         }
-        // one queue reservation per position, issued back to back (adding 0
-        // where the lane has no survivor), then the keys stored
+        // One queue reservation per position, issued back to back (adding 0
+        // where the lane has no survivor), then the survivors stored as
+        // (logit bits, id): the list owners build the keys of survivors
+        // only, where here every slot would pay for it.  A lane whose
+        // survivors do not all fit stores none and flags the overflow, which
+        // sends the whole tile down the full path.
         int base[C::TR];
 #pragma unroll
         for (int y = 0; y < C::TR; ++y) base[y] = atomicAdd(&s_cnt[wr * C::WR + y * 16 + l15], cnt[y]);
+        uint2* const sq2 = reinterpret_cast<uint2*>(sq);
 #pragma unroll
         for (int y = 0; y < C::TR; ++y) {
           const int p = wr * C::WR + y * 16 + l15;
-          if (cnt[y] == 1) {  // the only survivor is the largest logit
-            if (base[y] < C::QCAP) sq[p * C::QCAP + base[y]] = make_key(mx[y], static_cast<uint32_t>(vl0 + last[y]));
-            else s_flag[0] = 1;
-          } else if (cnt[y] > 1) {
+          const bool fits = base[y] + cnt[y] <= C::QCAP;
+          if (!fits) s_flag[0] = 1;
+          if (fits && cnt[y] == 1) {  // the only survivor is the largest logit
+            sq2[qslot(p, base[y])] = make_uint2(__float_as_uint(mx[y]), static_cast<uint32_t>(vl0 + last[y]));
+          } else if (fits && cnt[y] > 1) {
             int idx = base[y];
 #pragma unroll
             for (int x = 0; x < C::TV; ++x)
 #pragma unroll
               for (int q = 0; q < 4; ++q) {
                 if (acc[x][y][q] >= pt[y]) {
-                  if (idx < C::QCAP)
-                    sq[p * C::QCAP + idx] = make_key(acc[x][y][q], static_cast<uint32_t>(vl0 + x * 16 + q));
-                  else s_flag[0] = 1;
+                  sq2[qslot(p, idx)] = make_uint2(__float_as_uint(acc[x][y][q]), static_cast<uint32_t>(vl0 + x * 16 + q));
                   ++idx;
                 }
               }
@@ -721,7 +731,8 @@ __global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA /
         if (s_flag[0] == 0) {  // uniform: every thread reads the same flag
           const int n = min(s_cnt[ep], C::QCAP);
           for (int i = esub; i < n; i += C::TPP) {
-            const uint64_t key = sq[ep * C::QCAP + i];
+            const uint2 e = reinterpret_cast<const uint2*>(sq)[qslot(ep, i)];
+            const uint64_t key = make_key(__uint_as_float(e.x), e.y);
             if (key > list[KP - 1]) list_insert(list, key);
           }
 #pragma unroll
