@@ -470,17 +470,23 @@ __global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA /
     if constexpr (kRowThreshold) s_thr[ep * C::TPP + esub] = thr;
   };
 
-  // Filtered epilogue: the position's threshold for the next tile, the
-  // KP-th largest key of its two lists together (every list entry is a
-  // logit of the position, so the KP-th of any of them bounds the KP-th of
-  // the whole vocabulary from below); also clears the position's queue.
-  auto row_bound = [&]() {
-    float* const s_u = reinterpret_cast<float*>(smem + C::U_OFF);
+  // Filtered epilogue: the position's threshold for the tile, the KP-th
+  // largest key of its two lists together after the previous tile (every
+  // list entry is a logit of the position, so the KP-th of any of them bounds
+  // the KP-th of the whole vocabulary from below); the first owner also
+  // clears the position's queue counter there.
+  // The second list owner publishes its floors at the end of a tile; the
+  // first takes the bound at the start of the next tile's epilogue, before
+  // the barrier that opens it (the next tile's slice barriers order the two,
+  // so no barrier of its own is needed).
+  float* const s_u = reinterpret_cast<float*>(smem + C::U_OFF);
+  auto publish_floors = [&]() {
     if (esub == 1) {
 #pragma unroll
       for (int j = 0; j < KP; ++j) s_u[ep * 16 + j] = list_floor(list[j]);
     }
-    lds_sync();
+  };
+  auto take_bound = [&]() {
     if (esub == 0) {
       float a[KP], b[KP];
 #pragma unroll
@@ -591,6 +597,9 @@ __global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA /
         while (pend < kItems) consume_item(pend++);
       }
       continue;
+    }
+    if constexpr (kFilt) {
+      if (tl > 0) take_bound();  // published by the barrier below
     }
     float* sE;
     if constexpr (C::EPI_ALIAS) {
@@ -739,8 +748,8 @@ __global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA /
           for (int x = 0; x < C::TV; ++x)
 #pragma unroll
             for (int y = 0; y < C::TR; ++y) acc[x][y] = floatx4{0.f, 0.f, 0.f, 0.f};
-          row_bound();  // its barrier also ends every read of the queues
-          continue;     // the next tile's slices begin with a barrier
+          publish_floors();
+          continue;  // the next slice's barrier ends every read of the queues
         }
         // a queue overflowed: the whole tile takes the full path below
       }
@@ -784,7 +793,7 @@ __global__ __launch_bounds__(C::NTA) __attribute__((amdgpu_waves_per_eu(C::NTA /
     if constexpr (kFilt) {
       // thresholds for the next tile; counters and flag cleared (the flag
       // was read by every thread before the barriers above)
-      row_bound();
+      publish_floors();
       if (tid == 0) s_flag[0] = 0;
     }
   }
