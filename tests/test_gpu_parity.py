@@ -236,6 +236,8 @@ RAGGED = [
     # up to 32 rows the reduction runs in 256-wide slices: several slices
     # with a tail, exactly one slice, and many slices ending in an 8-wide tail
     (17, 328, 5000, 8), (32, 584, 70001, 8), (3, 256, 129, 4), (1, 4104, 3001, 8),
+    # the same tile's consumer wavefronts holding 16- and 32-key lists
+    (12, 136, 20000, 16), (24, 72, 9000, 24),
     # the large-row tile with 16 keys per list: the filtered epilogue
     (200, 136, 40000, 16), (513, 72, 9000, 16),
     # the large-row tile with 4-key lists (its seed is the 4th largest of 16
