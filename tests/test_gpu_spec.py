@@ -98,6 +98,10 @@ def _oracle_margins(logits, T, cid, prob, x, u, seed, row_ids):
     ("llada8b-b1-l32", 1.0, "candidates", 0),
     ("llada8b-b1-l32", 3.0, "uniform", 0),
     ("dream7b-b16-l32", 1.0, "candidates", 40),  # K + 1 = 17, flat rows; sampled rows
+    # the batched shapes the benchmark times: 8 and 16 row tiles of the
+    # large-row tile; sampled rows plus the first and last of every row tile
+    pytest.param("llada8b-b64-l32", 1.0, "candidates", 32, marks=pytest.mark.slow),
+    pytest.param("llada8b-b256-l16", 2.0, "uniform", 16, marks=pytest.mark.slow),
 ])
 def test_spec_decisions_match_oracle(name, T, law, n_sample):
     wl = _workload(name)
@@ -107,8 +111,13 @@ def test_spec_decisions_match_oracle(name, T, law, n_sample):
                             torch.from_numpy(prob).cuda(), torch.from_numpy(u).cuda(), seed, T)
     torch.cuda.synchronize()
     g = {k: v.cpu().numpy() for k, v in out.items()}
-    sel = (np.arange(wl.rows) if n_sample == 0 else
-           np.sort(np.random.default_rng(5).choice(wl.rows, n_sample, replace=False)))
+    if n_sample == 0:
+        sel = np.arange(wl.rows)
+    else:  # random rows, and the first and last row of every 256-row tile
+        edges = {t for t0 in range(0, wl.rows, 256) for t in (t0, min(t0 + 255, wl.rows - 1))}
+        picked = np.random.default_rng(5).choice(wl.rows, n_sample, replace=False).tolist()
+        sel = np.array(sorted(edges | set(picked)))
+    print(f"[spec] {name} T={T} law={law}: oracle on {len(sel)} of {wl.rows} rows", flush=True)
     Hb = synth.bf16_bits(Hv)[sel]
     logits = oracle.lm_logits(oracle.bf16_to_f64(Hb), synth.bf16_bits(blk.W))
     rs, sure_a, sure_r = _oracle_margins(logits, T, cid[sel], prob[sel], x.reshape(-1)[sel], u[sel], seed, sel)
