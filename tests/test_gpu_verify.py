@@ -63,12 +63,14 @@ def test_fused_pass_matches_separate_pass_and_oracle(wl_name, sample):
 
 
 @pytest.mark.slow
-def test_fused_pass_batched_shape():
-    """The fused pass at the shape the benchmark times for the 2048-row
-    workload: 2048 proposal rows and 2048 verifier rows in one launch (16 row
-    tiles of the large-row tile).  Checked on the first and last row of every
-    256-row tile of both halves, plus random rows."""
-    wl = synth.WORKLOADS["llada8b-b64-l32"]
+@pytest.mark.parametrize("wl_name", ["llada8b-b64-l32", "llada8b-b256-l16"])
+def test_fused_pass_batched_shape(wl_name):
+    """The fused pass at the shapes the benchmark times: 2048 (4096) proposal
+    rows and as many verifier rows in one launch, 16 (32) row tiles of the
+    large-row tile.  Checked on the first and last row of every 256-row tile
+    of both halves, plus random rows."""
+    _say(f"[fused pass] {wl_name}")
+    wl = synth.WORKLOADS[wl_name]
     blk = synth.make_block(wl, "cuda")
     Hv = _verifier_rows(blk, 0.3, 11)
     hidden = torch.cat([blk.H, Hv], dim=0).contiguous()
