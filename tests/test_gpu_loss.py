@@ -40,9 +40,13 @@ def _check(g, o):
 
 
 @pytest.mark.parametrize("name", ["tiny-d64-v512", "llada8b-b1-l32",
-                                  pytest.param("llada8b-b64-l32", marks=pytest.mark.slow)])
+                                  pytest.param("llada8b-b64-l32", marks=pytest.mark.slow),
+                                  pytest.param("dream7b-b16-l32", marks=pytest.mark.slow),
+                                  pytest.param("llada8b-b256-l16", marks=pytest.mark.slow)])
 def test_loss_matches_oracle(name):
-    _check(*_run(synth.WORKLOADS[name]))
+    g, o = _run(synth.WORKLOADS[name])
+    print(f"[loss] {name}: {o['count']} of {len(o['mask'])} positions reached", flush=True)
+    _check(g, o)
 
 
 @pytest.mark.parametrize("B,L,K,d,V", [(5, 7, 16, 136, 900), (33, 4, 5, 64, 300), (2, 40, 64, 72, 700)])
