@@ -1,6 +1,6 @@
 """GPU checks that no entry point writes outside the buffers it is given:
-every output and workspace is a view into a larger byte buffer whose guard
-bands (4 KiB on each side, filled with 0xA5) must be unchanged after the
+every output, workspace and table is a view into a larger byte buffer whose
+guard bands (4 KiB on each side, filled with 0xA5) must be unchanged after the
 call.  Shapes include ragged tails and the large-row tile."""
 import ctypes
 
@@ -92,6 +92,52 @@ def test_step_entry_points_stay_in_bounds(name, B, L, d, V, K):
                                 com.t.data_ptr(), ncom.t.data_ptr(), None)
     assert st == 0
     _check(acc2, com, ncom)
+
+
+@pytest.mark.parametrize("name,B,L,d,V,K", SHAPES)
+def test_tables_split_and_noalloc_entry_points_stay_in_bounds(name, B, L, d, V, K):
+    """The no-alloc propose, the per-token tables (brisk_corrector_prepare),
+    the rerank that reads them (on the 70-sequence shape the scan gathers the
+    table rows itself; with 64 keys the multi-wave scan runs) and the rerank
+    split at the candidates, each into guarded buffers."""
+    print(f"[canary] tables, split and no-alloc entries: {name} B={B} L={L} d={d} V={V} K={K}", flush=True)
+    wl, blk = _block(B, L, d, V, K, 13)
+    rows = B * L
+    L_ = brisk.lib()
+    cl, ci = Guarded((rows, K), torch.float32), Guarded((rows, K), torch.int32)
+    brisk.propose_block_noalloc(blk.H, blk.W, K, cl.t, ci.t)
+    _check(cl, ci)
+
+    corr = brisk.Corrector(blk.psi, blk.alpha, blk.b_g)
+    tb, wb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert L_.brisk_corrector_tables_size(ctypes.byref(corr.c_struct), V, ctypes.byref(tb), ctypes.byref(wb)) == 0
+    tab, wst = Guarded((tb.value // 4,), torch.float32), _ws(wb.value)
+    st = L_.brisk_corrector_prepare(ctypes.byref(corr.c_struct), blk.W.data_ptr(), blk.E.data_ptr(), V, d,
+                                    tab.t.data_ptr(), tb.value, wst.t.data_ptr(), wst.nbytes, None)
+    assert st == 0
+    _check(tab, wst)
+    corr.tables = tab.t
+    corr.c_struct.tables = tab.t.data_ptr()
+    corr.c_struct.tables_V = V
+
+    def outs():
+        return {"selected": Guarded((B, L), torch.int32), "refined": Guarded((rows, K), torch.float32),
+                "gamma": Guarded((rows,), torch.float32), "resid": Guarded((rows, K), torch.float32),
+                "accept_len": Guarded((B,), torch.int32), "correction": Guarded((B,), torch.int32)}
+
+    one, ws1 = outs(), _ws(brisk.rerank_workspace_size(corr, B, L, K))
+    brisk.rerank_verify(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl.t, ci.t, blk.verifier, B, L,
+                        workspace=ws1.t, **{k: g.t for k, g in one.items()})
+    _check(ws1, *one.values())
+
+    two, ws2 = outs(), _ws(ws1.nbytes)
+    brisk.rerank_hoist(corr, blk.H, blk.h_c, blk.x0, blk.E, B, L, K, ws2.t)
+    _check(ws2)
+    brisk.rerank_finish(corr, blk.H, blk.h_c, blk.x0, blk.W, blk.E, cl.t, ci.t, B, L, ws2.t,
+                        verifier=blk.verifier, **{k: g.t for k, g in two.items()})
+    _check(ws2, *two.values())
+    for k in one:
+        assert torch.equal(one[k].t, two[k].t), k
 
 
 @pytest.mark.parametrize("name,B,L,d,V,K", SHAPES)
