@@ -64,31 +64,74 @@ struct FillArgs {
   int rows, K, B, V, ds, vs;  // rows = B = 0: nothing to copy
 };
 
+// Vector n: the candidates' EH, TZ and TH rows first, then the anchors' TZ
+// and TH rows.  fill_id gives its token id; fill_vec its source, destination
+// and length for that id.
+struct FillVec {
+  const float* src;
+  float* dst;
+  int len;
+};
+__device__ __forceinline__ int fill_id(const FillArgs& a, int n) {
+  const int n_cand = a.rows * 3 * a.K;
+  if (n < n_cand) {
+    const int r = n / (3 * a.K), k = n % (3 * a.K) % a.K;
+    return clamp_id(a.cand_id[static_cast<size_t>(r) * a.K + k], a.V);
+  }
+  return clamp_id(a.anchor[(n - n_cand) % a.B], a.V);
+}
+__device__ __forceinline__ FillVec fill_vec(const FillArgs& a, int n, int v) {
+  const int n_cand = a.rows * 3 * a.K;
+  if (n < n_cand) {
+    const int r = n / (3 * a.K), f = n % (3 * a.K), kind = f / a.K;
+    return {a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs,
+            a.SB + (static_cast<size_t>(r) * (2 + 3 * a.K) + 2 + f) * a.vs, a.vs};
+  }
+  const int m = n - n_cand, b = m % a.B, kind = 1 + m / a.B;  // TZ, then TH
+  return {a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs,
+          (kind == 1 ? a.TZA : a.THA) + static_cast<size_t>(b) * a.ds, a.ds};
+}
+
+// A wavefront copies kFillBatch consecutive vectors at a time: lane g loads
+// vector g's token id (one load for the batch), then every lane loads its 16
+// bytes of each source row before the first store, so the batch waits for
+// two memory latencies instead of two per vector.  With 256-float table rows
+// (d_state <= 256) the row loads are unconditional (a table row is never
+// shorter) and only the stores into rows of d_state floats are masked; other
+// strides copy vector by vector.
+constexpr int kFillBatch = 4;
 __device__ void fill_rows(const FillArgs& a, int first, int step) {
   const int lane = threadIdx.x & 63;
-  const int n_cand = a.rows * 3 * a.K;
-  for (int n = first; n < n_cand + 2 * a.B; n += step) {
-    const float* src;
-    float* dst;
-    int len;
-    if (n < n_cand) {
-      const int r = n / (3 * a.K), f = n % (3 * a.K), kind = f / a.K, k = f % a.K;
-      const int v = clamp_id(a.cand_id[static_cast<size_t>(r) * a.K + k], a.V);
-      src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
-      dst = a.SB + (static_cast<size_t>(r) * (2 + 3 * a.K) + 2 + f) * a.vs;
-      len = a.vs;
-    } else {
-      const int m = n - n_cand, b = m % a.B, kind = 1 + m / a.B;  // TZ, then TH
-      const int v = clamp_id(a.anchor[b], a.V);
-      src = a.tables + (static_cast<size_t>(kind) * a.V + v) * a.vs;
-      dst = (kind == 1 ? a.TZA : a.THA) + static_cast<size_t>(b) * a.ds;
-      len = a.ds;
+  const int n_all = a.rows * 3 * a.K + 2 * a.B;
+  // the batch index is wave-uniform
+  for (int n0 = __builtin_amdgcn_readfirstlane(first * kFillBatch); n0 < n_all; n0 += step * kFillBatch) {
+    const int my_id = fill_id(a, min(n0 + min(lane, kFillBatch - 1), n_all - 1));
+    if (a.vs == 256 && (a.ds & 3) == 0) {
+      // named, not arrays, so that nothing is staged through memory; a batch
+      // past the last vector repeats it (the same bytes to the same place)
+      static_assert(kFillBatch == 4, "the batch below is written out for four vectors");
+      const FillVec f0 = fill_vec(a, min(n0 + 0, n_all - 1), __builtin_amdgcn_readlane(my_id, 0));
+      const FillVec f1 = fill_vec(a, min(n0 + 1, n_all - 1), __builtin_amdgcn_readlane(my_id, 1));
+      const FillVec f2 = fill_vec(a, min(n0 + 2, n_all - 1), __builtin_amdgcn_readlane(my_id, 2));
+      const FillVec f3 = fill_vec(a, min(n0 + 3, n_all - 1), __builtin_amdgcn_readlane(my_id, 3));
+      const float4 v0 = *reinterpret_cast<const float4*>(f0.src + lane * 4);
+      const float4 v1 = *reinterpret_cast<const float4*>(f1.src + lane * 4);
+      const float4 v2 = *reinterpret_cast<const float4*>(f2.src + lane * 4);
+      const float4 v3 = *reinterpret_cast<const float4*>(f3.src + lane * 4);
+      if (lane * 4 < f0.len) *reinterpret_cast<float4*>(f0.dst + lane * 4) = v0;
+      if (lane * 4 < f1.len) *reinterpret_cast<float4*>(f1.dst + lane * 4) = v1;
+      if (lane * 4 < f2.len) *reinterpret_cast<float4*>(f2.dst + lane * 4) = v2;
+      if (lane * 4 < f3.len) *reinterpret_cast<float4*>(f3.dst + lane * 4) = v3;
+      continue;
     }
-    if ((len & 3) == 0) {
-      for (int e = lane * 4; e < len; e += 256)
-        *reinterpret_cast<float4*>(dst + e) = *reinterpret_cast<const float4*>(src + e);
-    } else {
-      for (int e = lane; e < len; e += 64) dst[e] = src[e];
+    for (int g = 0; g < kFillBatch && n0 + g < n_all; ++g) {
+      const FillVec f = fill_vec(a, n0 + g, __builtin_amdgcn_readlane(my_id, g));
+      if ((f.len & 3) == 0) {
+        for (int e = lane * 4; e < f.len; e += 256)
+          *reinterpret_cast<float4*>(f.dst + e) = *reinterpret_cast<const float4*>(f.src + e);
+      } else {
+        for (int e = lane; e < f.len; e += 64) f.dst[e] = f.src[e];
+      }
     }
   }
 }
@@ -1420,8 +1463,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   // 256 x 16, so the scan gathers from 64 sequences on.
   const bool scan_gathers = tab && pc && K <= 8 && B >= 64;
   // Without it the scan reads whole step blocks and the table rows are
-  // copied in, a wavefront per row.  Up to 4096 rows (4 MiB) the projection
-  // launch copies them, two rows a wavefront at most, which saves a launch
+  // copied in, kFillBatch rows a wavefront at a time.  Up to 4096 rows
+  // (4 MiB) the projection launch copies them, which saves a launch
   // (32 rows: 2.5 us of a rerank's 43); more would stretch that launch
   // (512 x 16 rows: 24 us against 15 + 8 us for two launches).
   const size_t vsz = step_vec_stride(ds);
@@ -1432,7 +1475,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   const FillArgs fargs{c.tables, cand_id, anchor_tok, SB, F(lay.TZA), F(lay.THA), fill ? rows : 0, K,
                        fill ? B : 0, V, ds, static_cast<int>(vsz)};
   if (fill_here) pj.fill = fargs;
-  const int fill_x = fill_here ? std::min(((n_vec + 7) / 8 + S - 1) / S, (4096 + S - 1) / S) : 0;
+  const int fill_x =
+      fill_here ? std::min(((n_vec + 4 * kFillBatch - 1) / (4 * kFillBatch) + S - 1) / S, (4096 + S - 1) / S) : 0;
   const int gx = std::max(max_tiles, std::max(cross_x, fill_x));
   const int gy = kMaxProjJobs + (fill_here ? 2 : 1);  // the table-row row only when it copies
   if (gx > 0) {
@@ -1441,7 +1485,8 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
     else
       hipLaunchKernelGGL(gather_proj_kernel<64>, dim3(gx, gy, S), dim3(256), 0, s, pj);
   }
-  if (fill && !fill_here) hipLaunchKernelGGL(fill_kernel, dim3((n_vec + 3) / 4), dim3(256), 0, s, fargs);
+  if (fill && !fill_here)
+    hipLaunchKernelGGL(fill_kernel, dim3((n_vec + 4 * kFillBatch - 1) / (4 * kFillBatch)), dim3(256), 0, s, fargs);
 
   if (S > 1) {
     SliceArrs sl{};
