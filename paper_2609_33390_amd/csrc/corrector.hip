@@ -178,8 +178,8 @@ __device__ __forceinline__ float dot8_bf16(uint4 a, uint4 c, float s) {
 
 // G candidates a wavefront at most, U 512-element chunks of each operand in
 // flight per lane.  One candidate a wavefront takes eight chunks, so a 4096-
-// long dot is one round of loads instead of four (the accumulation order
-// over k is the same).
+// long dot is one round of loads instead of four, and groups of four take
+// four chunks, two rounds (the accumulation order over k is the same).
 template <int G, int U>
 __device__ void cross_dots(const CrossJob& cj, int d) {
   const int lane = threadIdx.x & 63;
@@ -250,6 +250,7 @@ __global__ __launch_bounds__(256) void gather_proj_kernel(ProjJobs jobs) {
   const int d = jobs.d;
   if (blockIdx.y == kMaxProjJobs) {
     if (jobs.cross.group == 1) cross_dots<1, 8>(jobs.cross, d);
+    else if (jobs.cross.group == 4) cross_dots<4, 4>(jobs.cross, d);
     else cross_dots<8, 2>(jobs.cross, d);
     return;
   }
@@ -1442,7 +1443,14 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
     const int t = proj_tiles(pj.job[j].n, pj.job[j].J, bj);
     max_tiles = t > max_tiles ? t : max_tiles;
   }
-  const int group = NC >= 4096 ? 8 : 1;
+  // Candidates per cross-logit wavefront.  Below 4096 dots, one (more
+  // wavefronts win).  Up to 32768 the gather waits on latency: groups of
+  // four with four chunks in flight (two rounds of loads per 4096-long dot)
+  // took 83-85 against 90-93 us after the LM-head launch at 2048 rows x 8
+  // keys and 92 against 97 us at 512 x 16.  From 32768 dots (268 MB of
+  // lm_head rows at 4096 x 8) it streams near the HBM limit, and groups of
+  // eight, which read each hidden row half as often, were 2 us faster.
+  const int group = NC >= 32768 ? 8 : NC >= 4096 ? 4 : 1;
   // (no sequences: no cross logits in the hoisted part)
   pj.cross = CrossJob{lm_head, hidden, cand_id, anchor_tok, finish ? B : 0, L, K, V, F(lay.X), group};
   // the cross-logit row needs a wavefront per row and group of candidates,
