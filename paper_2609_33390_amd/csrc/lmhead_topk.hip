@@ -945,8 +945,8 @@ __device__ __forceinline__ void fold_parts(uint64_t (&list)[KP], const uint64_t*
 
 // Rows below rows_prop are proposal rows (K candidates out); the rows after
 // them are verifier rows, whose argmax (the top key) goes to ver_token.
-// NW wavefronts per row: four when there are many parts, one when a row has
-// at most 64 (the batched shapes), which needs no cross-wave stage.
+// NW wavefronts per row: one when a row has at most 256 parts (each lane
+// folds up to four, and no cross-wave stage is needed), four above that.
 template <int KP, int NW>
 __global__ __launch_bounds__(64 * NW) void topk_merge_kernel(const uint64_t* __restrict__ partial,
                                                              int rows, int n_keys, int K, int rows_prop,
@@ -1268,7 +1268,7 @@ void launch_kp_pass(const Plan& p, const uint16_t* H, const uint16_t* W, int row
 template <int KP>
 void launch_kp_merge(const Plan& p, int rows, int K, int rows_prop, const uint64_t* partial,
                      float* cand_logit, int32_t* cand_id, int32_t* ver_token, hipStream_t s) {
-  if (p.n_parts <= kWave)
+  if (p.n_parts <= 4 * kWave)
     hipLaunchKernelGGL((topk_merge_kernel<KP, 1>), dim3(rows), dim3(kWave), 0, s, partial, rows,
                        p.n_parts * KP, K, rows_prop, cand_logit, cand_id, ver_token);
   else
