@@ -1549,9 +1549,13 @@ void launch_rerank(const brisk_corrector& c, const uint16_t* hidden, const uint1
   int lift_rows = 0;
   for (int j = 0; j < kMaxLiftJobs; ++j) lift_rows = lj.job[j].n > lift_rows ? lj.job[j].n : lift_rows;
   const dim3 lift_grid((lift_rows + LT_BN - 1) / LT_BN, (lift_cols + LT_BJ - 1) / LT_BJ, kMaxLiftJobs);
-  // the candidate jobs' tiles: more than two per compute unit -> one buffer
-  // (the same choice in both parts of a split rerank)
-  const bool many_tiles = 3 * ((n_cand + LT_BN - 1) / LT_BN) * ((ds + LT_BJ - 1) / LT_BJ) > 512;
+  // Tiles of the candidate jobs and of the two hidden-state jobs: two or
+  // more per compute unit -> one buffer, which fits twice as many
+  // workgroups (the same choice in both parts of a split rerank).  At 4096
+  // rows with the tables, 512 hidden-state tiles: the step after the LM-head
+  // launch took 112.7 against 115.5 us with one buffer.
+  const bool many_tiles =
+      (3 * ((n_cand + LT_BN - 1) / LT_BN) + 2 * ((rows + LT_BN - 1) / LT_BN)) * ((ds + LT_BJ - 1) / LT_BJ) >= 512;
   if (lift_rows > 0) {
     if (many_tiles) hipLaunchKernelGGL(lift_kernel<1>, lift_grid, dim3(256), 0, s, lj);
     else hipLaunchKernelGGL(lift_kernel<2>, lift_grid, dim3(256), 0, s, lj);
