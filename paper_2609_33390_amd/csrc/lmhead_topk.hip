@@ -963,7 +963,19 @@ __global__ __launch_bounds__(64 * NW) void topk_merge_kernel(const uint64_t* __r
 #pragma unroll
   for (int j = 0; j < KP; ++j) list[j] = 0;
   fold_parts(list, src, n_keys / KP, tid, NT);
-  wave_merge(list);
+  if constexpr (NW == 1) {
+    // parts sit in lanes 0..n_parts-1 (and their repeats 64 apart); levels
+    // past the highest occupied lane group would merge empty lists
+    const int n_parts = n_keys / KP;
+    butterfly_merge<1>(list);
+    butterfly_merge<2>(list);
+    butterfly_merge<4>(list);
+    butterfly_merge<8>(list);
+    if (n_parts > 16) butterfly_merge<16>(list);
+    if (n_parts > 32) butterfly_merge<32>(list);
+  } else {
+    wave_merge(list);
+  }
   if constexpr (NW == 4) {
     if (lane == 0) {
 #pragma unroll
