@@ -258,6 +258,30 @@ def test_propose_ragged(rows, d, V, K):
     check_candidates(cl.cpu().numpy(), ci.cpu().numpy(), ol)
 
 
+# The merge's single wavefront stops its butterfly at the lanes that hold
+# parts (one part per lane up to 64): on the 256-row tile with V = 256 n,
+# 4096 rows give n parts per row for n <= 16, 2048 rows for n <= 32 and 1024
+# rows for n <= 64, so these cases sit on each side of the 16- and 32-part
+# boundaries.
+MERGE_PARTS = [(4096, 1), (4096, 15), (4096, 16), (2048, 17), (2048, 31), (2048, 32), (1024, 33)]
+
+
+@pytest.mark.parametrize("K", [8, 16])
+@pytest.mark.parametrize("rows,n", MERGE_PARTS)
+def test_propose_merge_part_counts(rows, n, K):
+    d, V = 64, 256 * n
+    _say(f"[merge parts] rows={rows} V={V} ({n} parts) K={K}")
+    g = torch.Generator(device="cpu").manual_seed(rows + n + K)
+    H = torch.randn(rows, d, generator=g).to(torch.bfloat16)
+    W = (torch.randn(V, d, generator=g) * 0.05).to(torch.bfloat16)
+    cl, ci = brisk.propose_block(H.to(DEV), W.to(DEV), K)
+    torch.cuda.synchronize()
+    rs = tile_rows(rows, n=128, seed=n)
+    ol = oracle.lm_logits(oracle.bf16_to_f64(synth.bf16_bits(H)[rs]), synth.bf16_bits(W))
+    check_candidates(cl.cpu().numpy()[rs], ci.cpu().numpy()[rs], ol)
+    check_gpu_order(cl.cpu().numpy(), ci.cpu().numpy())
+
+
 @pytest.mark.parametrize("K", [8, 16])
 @pytest.mark.parametrize("order", ["rising", "falling"])
 def test_propose_monotone_logits(order, K):
