@@ -357,7 +357,10 @@ REL_GATE = 2e-5
     (30, 40, 16, 136, 900, 320, 0.3, REL_GATE),
     # 130 sequences with K <= 8: with the tables, the single-wave scan gathers
     # the table rows itself instead of reading copied step blocks
-    (130, 5, 6, 72, 900, 96, 0.3, 0.0)])
+    (130, 5, 6, 72, 900, 96, 0.3, 0.0),
+    # cross logits in partial groups: 4200 candidates take groups of four
+    # (K = 5: four and one), 34560 groups of eight (K = 6: six)
+    (42, 20, 5, 72, 700, 32, 0.3, 0.0), (180, 32, 6, 64, 700, 32, 0.3, 0.0)])
 def test_rerank_ragged(B, L, K, d, V, r, psi, rel, tables):
     wl = synth.Workload("ragged", B=B, L=L, d=d, V=V, K=K, r=r, sigma=0.3, flat_frac=0.5, seed=B + L + K)
     blk = synth.make_block(wl, "cpu", psi_std=psi)
